@@ -1,0 +1,150 @@
+/*
+ * delta_attn.h — C ABI of the DELTA decode-step attention hot path on MI355X (gfx950).
+ *
+ * DELTA (arXiv 2510.09883) keeps the whole KV cache resident and splits the layers of one
+ * decoding step into three roles (App. A, Alg. 1):
+ *   FULL   decode attention over every cached token (Sec. 2, Eq. gqa_attention);
+ *   DELTA  the same full attention, whose softmax weights are then turned into token scores
+ *          (largest weight over all query heads), summed per page, and used to keep the last
+ *          L pages plus the top-(K-L) older pages (Sec. 4 "Selection mechanism" and
+ *          "Page-based DELTA"; App. A, Alg. 2);
+ *   SPARSE decode attention restricted to the selected pages (App. A, Alg. 1).
+ *
+ * Conventions shared by every entry point
+ *   Memory.   Structs, the `roles` array and the per-layer pointer arrays of delta_decode_step
+ *             are HOST memory.  Every other pointer is DEVICE memory owned by the caller.  The
+ *             library never allocates, frees, keeps a pointer, or synchronises `stream`
+ *             (a hipStream_t passed as void*; NULL = the default stream).  All work is
+ *             enqueued on `stream` in order.
+ *   Errors.   Every call returns a status (DELTA_OK = 0, negative on error).  All argument
+ *             checks run on the host before anything is enqueued, so a call that returns an
+ *             error has enqueued nothing and left every output untouched.  DELTA_ERR_HIP means
+ *             a launch was rejected by the HIP runtime.
+ *   Device-side preconditions (not checked): page-table entries name pages that exist;
+ *             1 <= seq_lens[b] <= max_seq_len; inputs are finite; selected indices were made by
+ *             delta_delta_attn_select for the same shape and selection parameters.
+ *   Layouts.  bf16 = IEEE bfloat16 bits.  q, out: [batch, n_q_heads, head_dim].
+ *             k_cache, v_cache: [n_phys_pages, n_kv_heads, page_size, head_dim] (one contiguous
+ *             page_size x head_dim tile per page and KV head).
+ *             page_table: int32 [batch, max_pages_per_seq], logical page -> physical page.
+ *             Query head j reads KV head j / (n_q_heads / n_kv_heads).
+ *   Numerics. bf16 inputs, fp32 accumulation and online softmax, bf16 round-to-nearest-even
+ *             outputs.  Results are deterministic: the same inputs and shape give bitwise
+ *             identical outputs, and a DELTA layer's attention output is bitwise identical to
+ *             delta_full_attn's on the same inputs.
+ *   Workspace. `ws` is caller-owned device memory of at least delta_workspace_bytes() bytes.
+ *             It must be zero-filled once after allocation; every call leaves it ready for the
+ *             next call.  Calls that share one workspace must not run concurrently.
+ */
+#ifndef DELTA_ATTN_H
+#define DELTA_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  DELTA_OK = 0,
+  DELTA_ERR_INVALID_ARG = -1,  /* null pointer, inconsistent sizes, L >= K, ...            */
+  DELTA_ERR_UNSUPPORTED = -2,  /* valid but not built: head_dim, group size, page size      */
+  DELTA_ERR_WORKSPACE = -3,    /* ws_bytes smaller than delta_workspace_bytes()             */
+  DELTA_ERR_HIP = -4           /* the HIP runtime rejected a launch                          */
+};
+
+enum { DELTA_ROLE_FULL = 0, DELTA_ROLE_DELTA = 1, DELTA_ROLE_SPARSE = 2 };
+
+/* Token score aggregation over query heads.  MAX is the paper's rule (Sec. 4 "Selection
+ * mechanism"; App. A, Alg. 2); SUM is offered as an alternative. */
+enum { DELTA_AGG_MAX = 0, DELTA_AGG_SUM = 1 };
+
+/* Problem shape of one layer (Sec. 2: m query heads, g KV groups, d_head). */
+typedef struct {
+  int32_t batch;              /* B >= 1                                                      */
+  int32_t n_q_heads;          /* m, a multiple of n_kv_heads                                  */
+  int32_t n_kv_heads;         /* g; supported group sizes m/g: 1..8                           */
+  int32_t head_dim;           /* d_head: 64 or 128                                            */
+  int32_t page_size;          /* P: must be 16 (Sec. 5 "Implementation details")             */
+  int32_t max_pages_per_seq;  /* row length of page_table                                     */
+  int32_t max_seq_len;        /* host upper bound of seq_lens[b]; sizes grids and workspace  */
+  float sm_scale;             /* softmax scale; 0 selects 1/sqrt(head_dim) (Eq. gqa_attention) */
+} delta_shape_t;
+
+/* One layer's paged KV cache (Sec. 4 "Page-based DELTA"; never evicted, Sec. 4). */
+typedef struct {
+  const void* k_cache;        /* bf16 [n_phys_pages, n_kv_heads, page_size, head_dim]         */
+  const void* v_cache;        /* bf16, same layout                                            */
+  const int32_t* page_table;  /* int32 [batch, max_pages_per_seq]                             */
+  const int32_t* seq_lens;    /* int32 [batch]: tokens cached, the current one included       */
+} delta_kv_t;
+
+/* Selection parameters (Sec. 4; App. A, Alg. 2).  All counts are in TOKENS and must be whole
+ * units: budget k = K*U, recency window l = L*U.  unit_tokens U = 16 is page-based DELTA (the
+ * paper's configuration); U = 1 is the token-level rule of Sec. 4. */
+typedef struct {
+  int32_t budget_tokens;      /* k: tokens kept per sequence, a multiple of U, > recent       */
+  int32_t recent_tokens;      /* l: most recent tokens always kept, a multiple of U, >= 0     */
+  int32_t unit_tokens;        /* U: 16 (pages) or 1 (tokens)                                  */
+  int32_t agg;                /* DELTA_AGG_MAX (paper) or DELTA_AGG_SUM                       */
+} delta_select_t;
+
+/* Bytes of workspace needed by every call with this shape (and, if non-NULL, these selection
+ * parameters; pass the same `sel` used for DELTA and SPARSE calls).  Host only. */
+int delta_workspace_bytes(const delta_shape_t* shape, const delta_select_t* sel, size_t* out);
+
+/* Zero-fills `ws_bytes` bytes of `ws` on `stream` with a kernel (safe under stream capture).
+ * Equivalent to allocating the workspace zero-filled. */
+int delta_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/* FULL role: out[b, j, :] = sum_t softmax_t(sm_scale * q[b,j].k_t) v_t over all seq_lens[b]
+ * tokens of sequence b, k_t/v_t read from KV head j / G (Sec. 2, Eq. gqa_attention;
+ * App. A, Alg. 1 full branch).  One kernel launch.
+ *   q:   bf16 [B, m, d]   out: bf16 [B, m, d] */
+int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q, void* out,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* DELTA role: the FULL computation (bitwise-identical `out`), then RefreshPages (App. A,
+ * Alg. 2): token score s_t = max over all m heads of softmax weight (Sec. 4), unit score
+ * S_u = sum of s_t over the U tokens of unit u (a partial last unit sums the tokens it has),
+ * and the selected set = the last L units plus the top-(K-L) of the older units by S_u,
+ * equal scores taken lower index first.  When a sequence has n_u <= K units, all are kept.
+ *   sel_idx:     int32 [B, K] (K = budget_tokens / U): the selected logical unit indices of
+ *                each sequence in ascending order; entries at and past sel_cnt[b] are -1.
+ *   sel_cnt:     int32 [B]: min(K, ceil(seq_lens[b] / U)).
+ *   unit_scores: optional fp32 [B, ceil(max_seq_len / U)]: S_u for u < ceil(seq_lens[b]/U);
+ *                NULL keeps them in the workspace. */
+int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
+                            void* out, const delta_select_t* sel, int32_t* sel_idx,
+                            int32_t* sel_cnt, float* unit_scores, void* ws, size_t ws_bytes,
+                            void* stream);
+
+/* SPARSE role: attention of each query over the tokens of the selected units only, the
+ * softmax renormalised over them (App. A, Alg. 1 sparse branch).  Unit u covers tokens
+ * [u*U, min(u*U + U, seq_lens[b])).  sel_idx / sel_cnt as produced by
+ * delta_delta_attn_select with the same `sel`.  One kernel launch. */
+int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
+                      void* out, const delta_select_t* sel, const int32_t* sel_idx,
+                      const int32_t* sel_cnt, void* ws, size_t ws_bytes, void* stream);
+
+/* One decoding step over a layer stack (App. A, Alg. 1).  roles[i] in DELTA_ROLE_*; kv, q and
+ * out are HOST arrays of n_layers entries (q[i], out[i] device pointers as above).  The
+ * selected set starts as every unit; each DELTA layer writes its own slot
+ * sel_idx[d] ([B, K]) and sel_cnt[d] ([B]), d counting DELTA layers from 0, and every later
+ * SPARSE layer reads the most recent slot.  A SPARSE layer before the first DELTA layer
+ * attends to every unit, i.e. runs FULL.  sel may be NULL only if no layer is DELTA/SPARSE.
+ * Enqueues only kernels, so the whole step can be captured into a HIP graph. */
+int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                      const delta_kv_t* kv, const void* const* q, void* const* out,
+                      const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* delta_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DELTA_ATTN_H */

@@ -1,0 +1,403 @@
+// Split-K paged decode attention for gfx950, in three row modes (full / Delta / sparse).
+//
+// What it computes (Sec. 2, Eq. gqa_attention; App. A, Alg. 1): for sequence b and query
+// head j, out = sum_t softmax_t(scale * q_j . k_t) v_t over the rows of the sequence that the
+// mode selects, with k_t, v_t read from KV head j / G.  In Delta mode the scaled logits of
+// every token and the per-head log-sum-exp are also written, for the page scoring of
+// Sec. 4 ("Selection mechanism", "Page-based DELTA").
+//
+// Work decomposition.  One workgroup (4 waves) per (split, kv head g, sequence b).  A split
+// is a run of `gps` groups of 16 rows; a group is one 16-token page tile [16, D] of K and of
+// V (4 KB each at D = 128, contiguous in HBM), or 16 gathered token rows in token-level
+// sparse mode.  Waves take groups round-robin and keep their own online-softmax state, so
+// all G query heads of the KV group share every K/V byte read from HBM.
+//
+// Per group and wave:
+//   * QK^T on the matrix cores: v_mfma_f32_16x16x32_bf16 with A = the 16 K rows (M = rows,
+//     K = head dim) and B = the G query vectors padded to 16 columns; D/32 MFMAs give the
+//     16 x 16 score tile, lane l holding rows 4*(l/16)..+3 of head column l%16.
+//   * online softmax in the log2 domain (exp2, scale folded with log2 e); the group's
+//     probabilities and the per-head rescale factor go through a wave-private LDS slice;
+//   * P.V on the vector ALUs: each lane owns 8 consecutive head-dim columns of 16/RPI rows
+//     (128-bit loads, one V row per LPR consecutive lanes, fully coalesced).
+//   K/V of the next group are loaded before the current one is consumed (register double
+//   buffer) so every wave keeps 8 KB of loads in flight.
+//
+// Split combine.  The 4 waves merge through LDS into one (max, sum, o) partial per split,
+// written to the workspace.  The last workgroup of each (b, g) to arrive (device-scope fence +
+// atomic counter) merges the partials in split order — a fixed order, so results do not
+// depend on arrival order — writes bf16 outputs (and the log-sum-exp), and re-arms the
+// counter to zero for the next launch.
+#include "internal.h"
+
+namespace delta {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = kAttnThreads / 64;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ u32x4 load16(const uint16_t* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Compiler-level ordering for LDS traffic that stays inside one wave (the LDS unit executes
+// one wave's requests in order; this only stops the compiler from moving them).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int D>
+struct Geo {
+  static constexpr int NK = D / 32;     // MFMA k-steps = 16-byte K loads per lane per group
+  static constexpr int LPR = D / 8;     // lanes per V row
+  static constexpr int RPI = 64 / LPR;  // V rows per wave-wide load
+  static constexpr int NI = 16 / RPI;   // V loads per lane per group
+};
+
+template <int D>
+struct Tile {
+  u32x4 k[Geo<D>::NK];
+  u32x4 v[Geo<D>::NI];
+  uint32_t kmask;   // bit r: row r valid (rows of the MFMA A operand and of the score tile)
+};
+
+template <int D, int G, int MODE>
+__global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
+  using Gm = Geo<D>;
+  const int split = blockIdx.x;
+  const int g = blockIdx.y;
+  const int b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int quad = lane >> 4;   // score-tile rows 4*quad .. 4*quad+3
+  const int hcol = lane & 15;   // score-tile column = query head within the group
+  const int Hq = a.n_q_heads;
+  const int bg = b * a.n_kv_heads + g;
+
+  const int s_b = a.seq_lens[b];
+  int n_groups;
+  if (MODE == ROWS_DENSE) n_groups = (s_b + 15) >> 4;
+  else if (MODE == ROWS_SEL_PAGE) n_groups = a.sel_cnt[b];
+  else n_groups = (a.sel_cnt[b] + 15) >> 4;
+  // lengths beyond the host bound are clamped so that no access leaves the buffers
+  n_groups = max(0, min(n_groups, a.max_groups));
+  const int n_valid = (n_groups + a.gps - 1) / a.gps;
+
+  if (n_valid == 0) {  // nothing to attend to: defined output (zeros), log-sum-exp = -inf
+    if (split == 0) {
+      for (int i = tid; i < G * D; i += kAttnThreads)
+        a.out[((size_t)b * Hq + g * G) * D + i] = 0;
+      if (a.lse && tid < G) a.lse[(size_t)b * Hq + g * G + tid] = kNegInf;
+    }
+    return;
+  }
+  if (split >= n_valid) return;
+
+  const int g0 = split * a.gps;
+  const int ng = min(a.gps, n_groups - g0);
+
+  // ---- stage this split's page (or row) list in LDS -----------------------------------
+  __shared__ int s_rows[kMaxRowSlots];
+  __shared__ int s_aux[kMaxRowSlots];
+  const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
+  if (MODE == ROWS_DENSE) {
+    for (int i = tid; i < ng; i += kAttnThreads) {
+      s_rows[i] = pt[g0 + i];
+      s_aux[i] = min(16, s_b - 16 * (g0 + i));
+    }
+  } else if (MODE == ROWS_SEL_PAGE) {
+    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    for (int i = tid; i < ng; i += kAttnThreads) {
+      const int u = sel[g0 + i];
+      s_rows[i] = pt[u];
+      s_aux[i] = min(16, s_b - 16 * u);
+    }
+  } else {
+    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    const int cnt = min(a.sel_cnt[b], a.sel_stride);
+    for (int i = tid; i < 16 * ng; i += kAttnThreads) {
+      const int idx = 16 * g0 + i;
+      int packed = -1;
+      if (idx < cnt) {
+        const int t = sel[idx];
+        packed = pt[t >> 4] * 16 + (t & 15);
+      }
+      s_rows[i] = packed;
+    }
+  }
+  __syncthreads();
+
+  // ---- query operand (MFMA B: k = head dim, n = query head, zero-padded to 16) -----------
+  bf16x8 qb[Gm::NK];
+  {
+    const uint16_t* qp = a.q + ((size_t)b * Hq + g * G + min(hcol, G - 1)) * D + 8 * quad;
+#pragma unroll
+    for (int ks = 0; ks < Gm::NK; ++ks) {
+      u32x4 w = load16(qp + 32 * ks);
+      if (hcol >= G) w = u32x4{0u, 0u, 0u, 0u};
+      qb[ks] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  const size_t head_off = (size_t)g * 16 * D;
+  auto load_tile = [&](Tile<D>& t, int li) {
+    if (MODE == ROWS_SEL_TOKEN) {
+      // every row is its own (page, row); invalid rows re-read the group's first row
+      const int* rows = s_rows + 16 * li;
+      const int first = rows[0];
+      int kr = rows[hcol];
+      t.kmask = 0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t.kmask |= (rows[r] >= 0 ? 1u : 0u) << r;
+      if (kr < 0) kr = first;
+      const uint16_t* kp = a.k_cache + (size_t)(kr >> 4) * a.page_stride + head_off +
+                           (size_t)(kr & 15) * D + 8 * quad;
+#pragma unroll
+      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
+#pragma unroll
+      for (int i = 0; i < Gm::NI; ++i) {
+        int vr = rows[Gm::RPI * i + lane / Gm::LPR];
+        if (vr < 0) vr = first;
+        t.v[i] = load16(a.v_cache + (size_t)(vr >> 4) * a.page_stride + head_off +
+                        (size_t)(vr & 15) * D + 8 * (lane % Gm::LPR));
+      }
+    } else {
+      const size_t page = (size_t)s_rows[li] * a.page_stride + head_off;
+      const int nrows = s_aux[li];
+      t.kmask = (nrows >= 16) ? 0xffffu : ((1u << nrows) - 1u);
+      const uint16_t* kp = a.k_cache + page + (size_t)hcol * D + 8 * quad;
+#pragma unroll
+      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
+      const uint16_t* vp = a.v_cache + page + (size_t)(lane / Gm::LPR) * D + 8 * (lane % Gm::LPR);
+#pragma unroll
+      for (int i = 0; i < Gm::NI; ++i) t.v[i] = load16(vp + (size_t)Gm::RPI * i * D);
+    }
+  };
+
+  // wave-private LDS slice: P[16 rows][8 heads] and the per-head rescale factor
+  __shared__ float s_p[kWaves][16 * 8 + 8];
+  float* lp = s_p[wave];
+
+  float m_run = kNegInf, l_run = 0.f;   // per head hcol (valid for hcol < G)
+  float o[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+
+  const int Hq_row = b * Hq + g * G;
+  auto process = [&](const Tile<D>& t, int li) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < Gm::NK; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.k[ks]), qb[ks],
+                                                    acc, 0, 0, 0);
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
+    if (MODE == ROWS_DENSE && a.logits != nullptr && hcol < G) {
+      float* lg = a.logits + (size_t)(Hq_row + hcol) * a.logit_stride + 16 * (g0 + li) + 4 * quad;
+      *reinterpret_cast<f32x4*>(lg) = f32x4{x[0], x[1], x[2], x[3]};
+    }
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);          // finite: row 0 of a group always exists
+    const float alpha = exp2f(m_run - m_new);
+    float p[4], ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      p[r] = exp2f(x[r] - m_new);
+      ps += p[r];
+    }
+    ps += __shfl_xor(ps, 16);
+    ps += __shfl_xor(ps, 32);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+
+    wave_lds_sync();
+    if (hcol < G) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) lp[(4 * quad + r) * 8 + hcol] = p[r];
+      if (quad == 0) lp[128 + hcol] = alpha;
+    }
+    wave_lds_sync();
+
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float al = lp[128 + h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] *= al;
+    }
+#pragma unroll
+    for (int i = 0; i < Gm::NI; ++i) {
+      const int row = Gm::RPI * i + lane / Gm::LPR;
+      u32x4 w = t.v[i];
+      if (!((t.kmask >> row) & 1u)) w = u32x4{0u, 0u, 0u, 0u};   // rows past the end may hold NaN
+      float v[8];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        v[2 * c] = __uint_as_float(w[c] << 16);
+        v[2 * c + 1] = __uint_as_float(w[c] & 0xffff0000u);
+      }
+      const float* pr = lp + row * 8;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float ph = pr[h];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph, v[e], o[h][e]);
+      }
+    }
+  };
+
+  if (wave < ng) {
+    Tile<D> cur, nxt;
+    load_tile(cur, wave);
+    for (int li = wave; li < ng; li += kWaves) {
+      load_tile(nxt, min(li + kWaves, ng - 1));   // clamped prefetch keeps loads unconditional
+      process(cur, li);
+      cur = nxt;
+    }
+  }
+
+  // ---- reduce o over the lanes that share a head-dim chunk -------------------------------
+#pragma unroll
+  for (int off = Gm::LPR; off < 64; off <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] += __shfl_xor(o[h][e], off);
+
+  // ---- merge the 4 waves into one split partial ------------------------------------------
+  __shared__ float s_m[kWaves][kMaxGroup], s_l[kWaves][kMaxGroup];
+  __shared__ float s_o[kWaves][G][D];
+  if (quad == 0 && hcol < G) {
+    s_m[wave][hcol] = m_run;
+    s_l[wave][hcol] = l_run;
+  }
+  if (lane < Gm::LPR) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_o[wave][h][8 * lane + e] = o[h][e];
+  }
+  __syncthreads();
+
+  const size_t pbase = ((size_t)bg * a.n_split + split) * G;
+  for (int idx = tid; idx < G * D; idx += kAttnThreads) {
+    const int h = idx / D, dc = idx % D;
+    float M = kNegInf;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+    float O = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = (s_m[w][h] == kNegInf) ? 0.f : exp2f(s_m[w][h] - M);
+      O += f * s_o[w][h][dc];
+      L += f * s_l[w][h];
+    }
+    a.part_o[(pbase + h) * D + dc] = O;
+    if (dc == 0) {
+      a.part_ml[(pbase + h) * 2 + 0] = M;
+      a.part_ml[(pbase + h) * 2 + 1] = L;
+    }
+  }
+
+  // ---- last workgroup of (b, g) merges the splits -----------------------------------------
+  __threadfence();
+  __syncthreads();
+  __shared__ int s_last;
+  if (tid == 0) s_last = (atomicAdd(&a.counters[bg], 1) == n_valid - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  __shared__ float s_f[kMaxSplits][kMaxGroup];   // per split and head: exp2(m_c - M)
+  __shared__ float s_sl[kMaxSplits][kMaxGroup];  // per split and head: l_c
+  __shared__ float s_M[kMaxGroup], s_L[kMaxGroup];
+  const size_t cbase = (size_t)bg * a.n_split * G;
+  for (int i = tid; i < n_valid * G; i += kAttnThreads) {
+    const int c = i / G, h = i % G;
+    s_f[c][h] = a.part_ml[(cbase + (size_t)c * G + h) * 2 + 0];
+    s_sl[c][h] = a.part_ml[(cbase + (size_t)c * G + h) * 2 + 1];
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = kNegInf;
+    for (int c = 0; c < n_valid; ++c) M = fmaxf(M, s_f[c][tid]);
+    s_M[tid] = M;
+  }
+  __syncthreads();
+  for (int i = tid; i < n_valid * G; i += kAttnThreads) {
+    const int c = i / G, h = i % G;
+    s_f[c][h] = exp2f(s_f[c][h] - s_M[h]);
+  }
+  __syncthreads();
+  if (tid < G) {
+    float L = 0.f;
+    for (int c = 0; c < n_valid; ++c) L += s_f[c][tid] * s_sl[c][tid];
+    s_L[tid] = L;
+    if (a.lse) a.lse[(size_t)Hq_row + tid] = s_M[tid] + log2f(L);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < G * D; idx += kAttnThreads) {
+    const int h = idx / D, dc = idx % D;
+    float O = 0.f;
+    for (int c = 0; c < n_valid; ++c) O += s_f[c][h] * a.part_o[(cbase + (size_t)c * G + h) * D + dc];
+    a.out[(size_t)(Hq_row + h) * D + dc] = f32_to_bf16_rne(O / s_L[h]);
+  }
+  if (tid == 0) a.counters[bg] = 0;
+}
+
+template <int D, int G>
+hipError_t launch_dg(int mode, const AttnArgs& a, int batch, hipStream_t stream) {
+  const dim3 grid(a.n_split, a.n_kv_heads, batch), block(kAttnThreads);
+  switch (mode) {
+    case ROWS_DENSE: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_DENSE>), grid, block, 0, stream, a); break;
+    case ROWS_SEL_PAGE: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_PAGE>), grid, block, 0, stream, a); break;
+    case ROWS_SEL_TOKEN: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_TOKEN>), grid, block, 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(int group, int mode, const AttnArgs& a, int batch, hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_dg<D, 1>(mode, a, batch, stream);
+    case 2: return launch_dg<D, 2>(mode, a, batch, stream);
+    case 3: return launch_dg<D, 3>(mode, a, batch, stream);
+    case 4: return launch_dg<D, 4>(mode, a, batch, stream);
+    case 5: return launch_dg<D, 5>(mode, a, batch, stream);
+    case 6: return launch_dg<D, 6>(mode, a, batch, stream);
+    case 7: return launch_dg<D, 7>(mode, a, batch, stream);
+    case 8: return launch_dg<D, 8>(mode, a, batch, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention(int head_dim, int group, int mode, const AttnArgs& a, int batch,
+                            hipStream_t stream) {
+  if (head_dim == 128) return launch_d<128>(group, mode, a, batch, stream);
+  if (head_dim == 64) return launch_d<64>(group, mode, a, batch, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace delta

@@ -1,0 +1,341 @@
+// C ABI of the DELTA decode-step attention hot path: argument checks, workspace layout, split
+// planning, launches, and the layer-schedule driver of App. A, Alg. 1.
+//
+// Nothing here touches device memory directly or synchronises: every call validates on the
+// host, then enqueues kernels on the caller's stream.  Grid sizes come from host-side bounds
+// (max_seq_len, budget), and the kernels read the actual per-sequence lengths and selection
+// counts on the device, so no step needs a device-to-host round trip.
+#include <math.h>
+#include <stdlib.h>
+
+#include <algorithm>
+
+#include "../../include/delta_attn.h"
+#include "internal.h"
+
+namespace {
+
+using namespace delta;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Workgroups the attention launch aims for: several per CU on 256 CUs, so that the chip fills
+// and the ragged tail of one launch is short.  DELTA_ATTN_TARGET_WGS overrides it for tuning.
+int target_workgroups() {
+  static int v = [] {
+    const char* e = getenv("DELTA_ATTN_TARGET_WGS");
+    int x = e ? atoi(e) : 0;
+    return x > 0 ? x : 1024;
+  }();
+  return v;
+}
+
+// Minimum 16-row groups per split (per workgroup of 4 waves): two per wave.
+int min_groups_per_split() {
+  static int v = [] {
+    const char* e = getenv("DELTA_ATTN_MIN_GPS");
+    int x = e ? atoi(e) : 0;
+    return x > 0 ? x : 8;
+  }();
+  return v;
+}
+
+struct SplitPlan {
+  int n_split = 0;
+  int gps = 0;
+  int max_groups = 0;
+};
+
+// Splits per (sequence, kv head) and groups per split for a launch over at most `max_groups`
+// groups of 16 rows.  Deterministic in the shape, so a FULL and a DELTA call over the same
+// shape use the same plan (and give bitwise-identical outputs).
+bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
+  if (max_groups < 1) max_groups = 1;
+  int want = std::max(1, ceil_div(target_workgroups(), pairs));
+  int most = std::max(1, ceil_div(max_groups, min_groups_per_split()));
+  int n_split = std::min(std::min(want, most), kMaxSplits);
+  int gps = ceil_div(max_groups, n_split);
+  if (gps > slot_cap) gps = slot_cap;
+  n_split = ceil_div(max_groups, gps);
+  if (n_split > kMaxSplits) return false;
+  p->n_split = n_split;
+  p->gps = gps;
+  p->max_groups = max_groups;
+  return true;
+}
+
+struct Layout {
+  size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, total = 0;
+  int max_split = 0;
+  int logit_stride = 0;
+  int nu_stride = 0;
+  SplitPlan dense, sparse;
+  int sparse_mode = ROWS_SEL_PAGE;
+};
+
+int check_shape(const delta_shape_t* s) {
+  if (!s) return DELTA_ERR_INVALID_ARG;
+  if (s->batch < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->max_seq_len < 1 ||
+      s->max_pages_per_seq < 1 || !(s->sm_scale >= 0.f) || isinf(s->sm_scale))
+    return DELTA_ERR_INVALID_ARG;
+  if (s->n_q_heads % s->n_kv_heads != 0) return DELTA_ERR_INVALID_ARG;
+  if ((int64_t)s->max_seq_len > (int64_t)s->max_pages_per_seq * 16) return DELTA_ERR_INVALID_ARG;
+  if (s->page_size != 16) return DELTA_ERR_UNSUPPORTED;
+  if (s->head_dim != 64 && s->head_dim != 128) return DELTA_ERR_UNSUPPORTED;
+  const int G = s->n_q_heads / s->n_kv_heads;
+  if (G > kMaxGroup) return DELTA_ERR_UNSUPPORTED;
+  if ((int64_t)s->batch * s->n_q_heads > (1 << 24) || s->batch > 65535 || s->n_kv_heads > 65535)
+    return DELTA_ERR_UNSUPPORTED;
+  return DELTA_OK;
+}
+
+int check_select(const delta_select_t* sel) {
+  if (!sel) return DELTA_ERR_INVALID_ARG;
+  if (sel->unit_tokens != 16 && sel->unit_tokens != 1) return DELTA_ERR_UNSUPPORTED;
+  if (sel->agg != DELTA_AGG_MAX && sel->agg != DELTA_AGG_SUM) return DELTA_ERR_INVALID_ARG;
+  if (sel->budget_tokens < 1 || sel->recent_tokens < 0) return DELTA_ERR_INVALID_ARG;
+  if (sel->budget_tokens % sel->unit_tokens || sel->recent_tokens % sel->unit_tokens)
+    return DELTA_ERR_INVALID_ARG;
+  if (sel->recent_tokens >= sel->budget_tokens) return DELTA_ERR_INVALID_ARG;   // L < K
+  return DELTA_OK;
+}
+
+int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (sel && (rc = check_select(sel))) return rc;
+  const int pairs = s->batch * s->n_kv_heads;
+  const int G = s->n_q_heads / s->n_kv_heads;
+  if (!plan_split(pairs, ceil_div(s->max_seq_len, 16), kMaxRowSlots, &L->dense))
+    return DELTA_ERR_UNSUPPORTED;
+  L->max_split = L->dense.n_split;
+  if (sel) {
+    const int K = sel->budget_tokens / sel->unit_tokens;
+    if (sel->unit_tokens == 16) {
+      L->sparse_mode = ROWS_SEL_PAGE;
+      if (!plan_split(pairs, K, kMaxRowSlots, &L->sparse)) return DELTA_ERR_UNSUPPORTED;
+    } else {
+      L->sparse_mode = ROWS_SEL_TOKEN;
+      if (!plan_split(pairs, ceil_div(K, 16), kMaxRowSlots / 16, &L->sparse))
+        return DELTA_ERR_UNSUPPORTED;
+    }
+    L->max_split = std::max(L->max_split, L->sparse.n_split);
+  }
+  L->logit_stride = ceil_div(s->max_seq_len, 16) * 16;
+  size_t off = 0;
+  L->counters = off;  off = align_up(off + sizeof(int32_t) * pairs);
+  L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * 2);
+  L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * s->head_dim);
+  if (sel) {
+    L->nu_stride = ceil_div(s->max_seq_len, sel->unit_tokens);
+    L->logits = off;  off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads * L->logit_stride);
+    L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
+    L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
+  }
+  L->total = off;
+  return DELTA_OK;
+}
+
+int check_kv(const delta_kv_t* kv) {
+  if (!kv || !kv->k_cache || !kv->v_cache || !kv->page_table || !kv->seq_lens)
+    return DELTA_ERR_INVALID_ARG;
+  return DELTA_OK;
+}
+
+float scale_log2(const delta_shape_t* s) {
+  const float sc = s->sm_scale > 0.f ? s->sm_scale : 1.0f / sqrtf((float)s->head_dim);
+  return sc * 1.4426950408889634f;
+}
+
+AttnArgs base_args(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
+                   const Layout& L, char* ws, const SplitPlan& plan) {
+  AttnArgs a{};
+  a.k_cache = static_cast<const uint16_t*>(kv->k_cache);
+  a.v_cache = static_cast<const uint16_t*>(kv->v_cache);
+  a.page_table = kv->page_table;
+  a.seq_lens = kv->seq_lens;
+  a.q = static_cast<const uint16_t*>(q);
+  a.out = static_cast<uint16_t*>(out);
+  a.part_o = reinterpret_cast<float*>(ws + L.part_o);
+  a.part_ml = reinterpret_cast<float*>(ws + L.part_ml);
+  a.counters = reinterpret_cast<int32_t*>(ws + L.counters);
+  a.page_stride = (int64_t)s->n_kv_heads * 16 * s->head_dim;
+  a.n_q_heads = s->n_q_heads;
+  a.n_kv_heads = s->n_kv_heads;
+  a.max_pages = s->max_pages_per_seq;
+  a.logit_stride = L.logit_stride;
+  a.n_split = plan.n_split;
+  a.gps = plan.gps;
+  a.max_groups = plan.max_groups;
+  a.scale_log2 = scale_log2(s);
+  return a;
+}
+
+int hip_rc(hipError_t e) { return e == hipSuccess ? DELTA_OK : DELTA_ERR_HIP; }
+
+int run_full(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
+             const Layout& L, char* ws, hipStream_t st) {
+  AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
+  return hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, ROWS_DENSE, a,
+                                 s->batch, st));
+}
+
+int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
+              const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, float* uscores,
+              const Layout& L, char* ws, hipStream_t st) {
+  AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
+  a.logits = reinterpret_cast<float*>(ws + L.logits);
+  a.lse = reinterpret_cast<float*>(ws + L.lse);
+  int rc = hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, ROWS_DENSE, a,
+                                   s->batch, st));
+  if (rc) return rc;
+  ScoreArgs sa{};
+  sa.logits = a.logits;
+  sa.lse = a.lse;
+  sa.seq_lens = kv->seq_lens;
+  sa.unit_scores = uscores ? uscores : reinterpret_cast<float*>(ws + L.uscores);
+  sa.n_q_heads = s->n_q_heads;
+  sa.logit_stride = L.logit_stride;
+  sa.nu_stride = L.nu_stride;
+  sa.max_seq_len = s->max_seq_len;
+  rc = hip_rc(launch_score(sel->agg, sel->unit_tokens, sa, s->batch, st));
+  if (rc) return rc;
+  SelectArgs xa{};
+  xa.unit_scores = sa.unit_scores;
+  xa.seq_lens = kv->seq_lens;
+  xa.sel_idx = sel_idx;
+  xa.sel_cnt = sel_cnt;
+  xa.nu_stride = L.nu_stride;
+  xa.unit_tokens = sel->unit_tokens;
+  xa.budget_units = sel->budget_tokens / sel->unit_tokens;
+  xa.recent_units = sel->recent_tokens / sel->unit_tokens;
+  return hip_rc(launch_select(xa, s->batch, st));
+}
+
+int run_sparse(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
+               const delta_select_t* sel, const int32_t* sel_idx, const int32_t* sel_cnt,
+               const Layout& L, char* ws, hipStream_t st) {
+  AttnArgs a = base_args(s, kv, q, out, L, ws, L.sparse);
+  a.sel_idx = sel_idx;
+  a.sel_cnt = sel_cnt;
+  a.sel_stride = sel->budget_tokens / sel->unit_tokens;
+  return hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, L.sparse_mode, a,
+                                 s->batch, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+int delta_workspace_bytes(const delta_shape_t* shape, const delta_select_t* sel, size_t* out) {
+  if (!out) return DELTA_ERR_INVALID_ARG;
+  Layout L;
+  int rc = make_layout(shape, sel, &L);
+  if (rc) return rc;
+  *out = L.total;
+  return DELTA_OK;
+}
+
+int delta_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws && ws_bytes) return DELTA_ERR_INVALID_ARG;
+  return hip_rc(launch_fill_zero(ws, ws_bytes, static_cast<hipStream_t>(stream)));
+}
+
+int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q, void* out,
+                    void* ws, size_t ws_bytes, void* stream) {
+  Layout L;
+  int rc = make_layout(shape, nullptr, &L);
+  if (rc) return rc;
+  if ((rc = check_kv(kv))) return rc;
+  if (!q || !out || !ws) return DELTA_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
+  return run_full(shape, kv, q, out, L, static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+}
+
+int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
+                            void* out, const delta_select_t* sel, int32_t* sel_idx,
+                            int32_t* sel_cnt, float* unit_scores, void* ws, size_t ws_bytes,
+                            void* stream) {
+  if (!sel) return DELTA_ERR_INVALID_ARG;
+  Layout L;
+  int rc = make_layout(shape, sel, &L);
+  if (rc) return rc;
+  if ((rc = check_kv(kv))) return rc;
+  if (!q || !out || !ws || !sel_idx || !sel_cnt) return DELTA_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
+  return run_delta(shape, kv, q, out, sel, sel_idx, sel_cnt, unit_scores, L,
+                   static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+}
+
+int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
+                      void* out, const delta_select_t* sel, const int32_t* sel_idx,
+                      const int32_t* sel_cnt, void* ws, size_t ws_bytes, void* stream) {
+  if (!sel) return DELTA_ERR_INVALID_ARG;
+  Layout L;
+  int rc = make_layout(shape, sel, &L);
+  if (rc) return rc;
+  if ((rc = check_kv(kv))) return rc;
+  if (!q || !out || !ws || !sel_idx || !sel_cnt) return DELTA_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
+  return run_sparse(shape, kv, q, out, sel, sel_idx, sel_cnt, L, static_cast<char*>(ws),
+                    static_cast<hipStream_t>(stream));
+}
+
+int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                      const delta_kv_t* kv, const void* const* q, void* const* out,
+                      const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, void* ws,
+                      size_t ws_bytes, void* stream) {
+  if (n_layers < 0 || (n_layers > 0 && (!roles || !kv || !q || !out)) || !ws)
+    return DELTA_ERR_INVALID_ARG;
+  int n_delta = 0, n_sel_users = 0;
+  for (int i = 0; i < n_layers; ++i) {
+    if (roles[i] < DELTA_ROLE_FULL || roles[i] > DELTA_ROLE_SPARSE) return DELTA_ERR_INVALID_ARG;
+    n_delta += roles[i] == DELTA_ROLE_DELTA;
+    n_sel_users += roles[i] != DELTA_ROLE_FULL;
+  }
+  if (n_sel_users && !sel) return DELTA_ERR_INVALID_ARG;
+  if (n_delta && (!sel_idx || !sel_cnt)) return DELTA_ERR_INVALID_ARG;
+  Layout L;
+  int rc = make_layout(shape, n_sel_users ? sel : nullptr, &L);
+  if (rc) return rc;
+  if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
+  for (int i = 0; i < n_layers; ++i) {
+    if ((rc = check_kv(&kv[i]))) return rc;
+    if (!q[i] || !out[i]) return DELTA_ERR_INVALID_ARG;
+  }
+  char* w = static_cast<char*>(ws);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int K = sel ? sel->budget_tokens / sel->unit_tokens : 0;
+  const size_t slot = (size_t)shape->batch * K;
+  int cur = -1;   // most recent Delta slot; -1 = every unit (App. A, Alg. 1 initialisation)
+  for (int i = 0; i < n_layers; ++i) {
+    if (roles[i] == DELTA_ROLE_FULL || (roles[i] == DELTA_ROLE_SPARSE && cur < 0)) {
+      rc = run_full(shape, &kv[i], q[i], out[i], L, w, st);
+    } else if (roles[i] == DELTA_ROLE_DELTA) {
+      ++cur;
+      rc = run_delta(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
+                     sel_cnt + (size_t)cur * shape->batch, nullptr, L, w, st);
+    } else {
+      rc = run_sparse(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
+                      sel_cnt + (size_t)cur * shape->batch, L, w, st);
+    }
+    if (rc) return rc;
+  }
+  return DELTA_OK;
+}
+
+const char* delta_status_string(int status) {
+  switch (status) {
+    case DELTA_OK: return "ok";
+    case DELTA_ERR_INVALID_ARG: return "invalid argument";
+    case DELTA_ERR_UNSUPPORTED: return "unsupported shape or parameter";
+    case DELTA_ERR_WORKSPACE: return "workspace too small";
+    case DELTA_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+// Internal interface between the C ABI layer (delta_api.cpp) and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace delta {
+
+// How the 16-row groups an attention workgroup walks are formed.
+enum RowMode {
+  ROWS_DENSE = 0,      // group i = logical page i of the sequence (full / Delta layers)
+  ROWS_SEL_PAGE = 1,   // group i = selected page sel_idx[b, i]            (sparse, U = 16)
+  ROWS_SEL_TOKEN = 2,  // group i = selected tokens sel_idx[b, 16i .. 16i+15] (sparse, U = 1)
+};
+
+// Hard limits of the attention kernel's on-chip staging.
+constexpr int kAttnThreads = 256;        // 4 waves of 64
+constexpr int kMaxSplits = 64;           // split partials combined by the last workgroup
+constexpr int kMaxRowSlots = 1024;       // LDS slots staging a split's page / row list
+constexpr int kMaxGroup = 8;             // query heads per KV head (padded to 16 MFMA columns)
+
+struct AttnArgs {
+  const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
+  const uint16_t* v_cache;
+  const int32_t* page_table; // [B, max_pages]
+  const int32_t* seq_lens;   // [B]
+  const int32_t* sel_idx;    // [B, sel_stride] (sparse modes)
+  const int32_t* sel_cnt;    // [B]             (sparse modes)
+  const uint16_t* q;         // bf16 [B, Hq, D]
+  uint16_t* out;             // bf16 [B, Hq, D]
+  float* part_o;             // [B*Hkv, n_split, G, D]   un-normalised split outputs
+  float* part_ml;            // [B*Hkv, n_split, G, 2]   split (max, sum) in the log2 domain
+  int32_t* counters;         // [B*Hkv] arrival counters, zero between launches
+  float* logits;             // [B, Hq, logit_stride] log2-domain logits, or null
+  float* lse;                // [B, Hq] log2-domain log-sum-exp, or null
+  int64_t page_stride;       // elements per physical page = Hkv * 16 * D
+  int32_t n_q_heads, n_kv_heads, max_pages, sel_stride, logit_stride;
+  int32_t n_split, gps;      // splits per (b, kv head) and 16-row groups per split
+  int32_t max_groups;        // host bound on groups per sequence (n_split * gps >= it)
+  float scale_log2;          // sm_scale * log2(e)
+};
+
+hipError_t launch_attention(int head_dim, int group, int mode, const AttnArgs& a, int batch,
+                            hipStream_t stream);
+
+struct ScoreArgs {
+  const float* logits;       // [B, Hq, logit_stride]
+  const float* lse;          // [B, Hq]
+  const int32_t* seq_lens;   // [B]
+  float* unit_scores;        // [B, nu_stride]
+  int32_t n_q_heads, logit_stride, nu_stride, max_seq_len;
+};
+
+hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,
+                        hipStream_t stream);
+
+struct SelectArgs {
+  const float* unit_scores;  // [B, nu_stride]
+  const int32_t* seq_lens;   // [B]
+  int32_t* sel_idx;          // [B, budget_units]
+  int32_t* sel_cnt;          // [B]
+  int32_t nu_stride, unit_tokens, budget_units, recent_units;
+};
+
+hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream);
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace delta

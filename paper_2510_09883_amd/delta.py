@@ -1,0 +1,164 @@
+"""Python binding of libdelta_attn.so (ctypes; argument marshalling only).
+
+Every function has the name and argument order of the C entry point declared in
+include/delta_attn.h.  Tensors are passed by device pointer; the stream is torch's current
+stream.  A non-zero status raises DeltaError.  Importing this module raises ImportError if
+the library has not been built: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdelta_attn.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                      "(python -m paper_2510_09883_amd.build)")
+_lib = ctypes.CDLL(LIB_PATH)
+
+DELTA_OK, DELTA_ERR_INVALID_ARG, DELTA_ERR_UNSUPPORTED, DELTA_ERR_WORKSPACE, DELTA_ERR_HIP = 0, -1, -2, -3, -4
+DELTA_ROLE_FULL, DELTA_ROLE_DELTA, DELTA_ROLE_SPARSE = 0, 1, 2
+DELTA_AGG_MAX, DELTA_AGG_SUM = 0, 1
+
+EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
+            "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
+            "delta_status_string"]
+
+
+class delta_shape_t(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("max_seq_len", ctypes.c_int32), ("sm_scale", ctypes.c_float)]
+
+
+class delta_kv_t(ctypes.Structure):
+    _fields_ = [("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("page_table", ctypes.c_void_p), ("seq_lens", ctypes.c_void_p)]
+
+
+class delta_select_t(ctypes.Structure):
+    _fields_ = [("budget_tokens", ctypes.c_int32), ("recent_tokens", ctypes.c_int32),
+                ("unit_tokens", ctypes.c_int32), ("agg", ctypes.c_int32)]
+
+
+_P = ctypes.POINTER
+_vp = ctypes.c_void_p
+_lib.delta_workspace_bytes.argtypes = [_P(delta_shape_t), _P(delta_select_t), _P(ctypes.c_size_t)]
+_lib.delta_workspace_init.argtypes = [_vp, ctypes.c_size_t, _vp]
+_lib.delta_full_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _vp, ctypes.c_size_t, _vp]
+_lib.delta_delta_attn_select.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp,
+                                         _P(delta_select_t), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+_lib.delta_sparse_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _P(delta_select_t),
+                                   _vp, _vp, _vp, ctypes.c_size_t, _vp]
+_lib.delta_decode_step.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
+                                   _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
+                                   _vp, _vp, _vp, ctypes.c_size_t, _vp]
+_lib.delta_status_string.argtypes = [ctypes.c_int]
+_lib.delta_status_string.restype = ctypes.c_char_p
+for _n in EXPORTED[:-1]:
+    getattr(_lib, _n).restype = ctypes.c_int
+
+
+class DeltaError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn}: {delta_status_string(status)} ({status})")
+        self.status = status
+
+
+def delta_status_string(status: int) -> str:
+    return _lib.delta_status_string(status).decode()
+
+
+def _check(fn, status):
+    if status != DELTA_OK:
+        raise DeltaError(fn, status)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def make_shape(batch, n_q_heads, n_kv_heads, head_dim, max_pages_per_seq, max_seq_len,
+               sm_scale=0.0, page_size=16) -> delta_shape_t:
+    return delta_shape_t(batch, n_q_heads, n_kv_heads, head_dim, page_size, max_pages_per_seq,
+                         max_seq_len, sm_scale)
+
+
+def make_select(budget_tokens, recent_tokens, unit_tokens=16, agg=DELTA_AGG_MAX) -> delta_select_t:
+    return delta_select_t(budget_tokens, recent_tokens, unit_tokens, agg)
+
+
+def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
+    return delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr())
+
+
+def delta_workspace_bytes(shape: delta_shape_t, sel: delta_select_t | None = None) -> int:
+    n = ctypes.c_size_t(0)
+    _check("delta_workspace_bytes",
+           _lib.delta_workspace_bytes(ctypes.byref(shape), ctypes.byref(sel) if sel else None,
+                                      ctypes.byref(n)))
+    return n.value
+
+
+def delta_workspace_init(ws: torch.Tensor):
+    _check("delta_workspace_init", _lib.delta_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream()))
+
+
+def alloc_workspace(shape, sel=None, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace (uint8) large enough for every call with this shape/selection."""
+    return torch.zeros(delta_workspace_bytes(shape, sel), dtype=torch.uint8, device=device)
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def delta_full_attn(shape, kv: delta_kv_t, q, out, ws):
+    _check("delta_full_attn", _lib.delta_full_attn(ctypes.byref(shape), ctypes.byref(kv), _ptr(q),
+                                                   _ptr(out), _ptr(ws), _nbytes(ws), _stream()))
+
+
+def delta_delta_attn_select(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, unit_scores, ws):
+    _check("delta_delta_attn_select",
+           _lib.delta_delta_attn_select(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
+                                        ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt),
+                                        _ptr(unit_scores), _ptr(ws), _nbytes(ws), _stream()))
+
+
+def delta_sparse_attn(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, ws):
+    _check("delta_sparse_attn",
+           _lib.delta_sparse_attn(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
+                                  ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt), _ptr(ws),
+                                  _nbytes(ws), _stream()))
+
+
+class StepArgs:
+    """Host-side argument arrays of delta_decode_step, built once and reused every step."""
+
+    def __init__(self, shape, roles, kvs, qs, outs, sel, sel_idx, sel_cnt, ws):
+        n = len(roles)
+        self.shape = shape
+        self.n = n
+        self.roles = (ctypes.c_int32 * n)(*roles)
+        self.kvs = (delta_kv_t * n)(*kvs)
+        self.qs = (_vp * n)(*[q.data_ptr() for q in qs])
+        self.outs = (_vp * n)(*[o.data_ptr() for o in outs])
+        self.sel = sel
+        self.sel_idx, self.sel_cnt, self.ws = sel_idx, sel_cnt, ws
+        self._keep = (qs, outs)
+
+
+def delta_decode_step(args: StepArgs):
+    a = args
+    _check("delta_decode_step",
+           _lib.delta_decode_step(ctypes.byref(a.shape), a.n, a.roles, a.kvs, a.qs, a.outs,
+                                  ctypes.byref(a.sel) if a.sel is not None else None,
+                                  _ptr(a.sel_idx), _ptr(a.sel_cnt), _ptr(a.ws), _nbytes(a.ws),
+                                  _stream()))

@@ -1,0 +1,114 @@
+"""CPU tests of the C ABI library: it loads, exports every function include/delta_attn.h
+declares, and rejects bad arguments on the host before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "delta_attn.h")
+
+
+@pytest.fixture(scope="module")
+def D():
+    from paper_2510_09883_amd import delta
+    return delta
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(delta_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol(D):
+    names = declared_functions()
+    assert len(names) == 7
+    lib = ctypes.CDLL(D.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(D.EXPORTED) == names
+
+
+def test_status_strings(D):
+    assert D.delta_status_string(0) == "ok"
+    assert D.delta_status_string(-3) == "workspace too small"
+
+
+def shape(D, **kw):
+    s = dict(batch=2, n_q_heads=32, n_kv_heads=8, head_dim=128, max_pages_per_seq=512,
+             max_seq_len=8192)
+    s.update(kw)
+    return D.make_shape(**s)
+
+
+def test_workspace_sizes(D):
+    s = shape(D)
+    a = D.delta_workspace_bytes(s)
+    b = D.delta_workspace_bytes(s, D.make_select(2048, 128))
+    c = D.delta_workspace_bytes(s, D.make_select(2048, 128, unit_tokens=1))
+    # the Delta path adds fp32 logits [B, Hq, s] + log-sum-exp + unit scores
+    assert b >= a + 4 * 2 * 32 * 8192
+    assert c > b
+    assert a % 256 == 0 and b % 256 == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_kv_heads=5), -1),          # Hq % Hkv != 0
+    (dict(head_dim=96), -2),           # unsupported head dim
+    (dict(page_size=32), -2),          # page size must be 16
+    (dict(n_kv_heads=2), -2),          # group 16 > 8 not built
+    (dict(max_seq_len=8193), -1),      # more tokens than the page table holds
+    (dict(batch=0), -1),
+    (dict(sm_scale=-1.0), -1),
+])
+def test_shape_validation(D, kw, status):
+    with pytest.raises(D.DeltaError) as e:
+        D.delta_workspace_bytes(shape(D, **kw))
+    assert e.value.status == status
+
+
+@pytest.mark.parametrize("sel,status", [
+    ((2048, 2048), -1),                # L >= K (Sec. 5 requires L < K)
+    ((2048, 4096), -1),
+    ((2040, 128), -1),                 # budget not a whole number of pages
+    ((2048, 120), -1),                 # window not a whole number of pages
+    ((0, 0), -1),
+])
+def test_select_validation(D, sel, status):
+    with pytest.raises(D.DeltaError) as e:
+        D.delta_workspace_bytes(shape(D), D.make_select(*sel))
+    assert e.value.status == status
+    with pytest.raises(D.DeltaError):
+        D.delta_workspace_bytes(shape(D), D.make_select(2048, 128, unit_tokens=8))
+    with pytest.raises(D.DeltaError):
+        D.delta_workspace_bytes(shape(D), D.make_select(2048, 128, agg=2))
+
+
+def test_calls_reject_before_launch(D):
+    """Every error path returns before anything reaches the (absent) GPU."""
+    s = shape(D)
+    sel = D.make_select(2048, 128)
+    kv = D.delta_kv_t(1, 2, 3, 4)          # fake device pointers: never dereferenced
+    lib = D._lib
+    P = ctypes.byref
+    need = D.delta_workspace_bytes(s, sel)
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.delta_full_attn(P(s), P(kv), fake, fake, fake, 16, None) == -3
+    assert lib.delta_full_attn(P(s), None, fake, fake, fake, need, None) == -1
+    assert lib.delta_full_attn(P(s), P(kv), None, fake, fake, need, None) == -1
+    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, P(sel), None, fake, None, fake, need, None) == -1
+    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, None, fake, fake, None, fake, need, None) == -1
+    assert lib.delta_sparse_attn(P(s), P(kv), fake, fake, P(sel), fake, fake, fake, need - 1, None) == -3
+    bad = D.make_shape(2, 32, 8, 80, 512, 8192)
+    assert lib.delta_full_attn(P(bad), P(kv), fake, fake, fake, need, None) == -2
+    roles = (ctypes.c_int32 * 3)(0, 1, 2)
+    kvs = (D.delta_kv_t * 3)(kv, kv, kv)
+    ptrs = (ctypes.c_void_p * 3)(0x1000, 0x1000, 0x1000)
+    # a Delta/sparse role needs selection parameters and selection buffers
+    assert lib.delta_decode_step(P(s), 3, roles, kvs, ptrs, ptrs, None, fake, fake, fake, need, None) == -1
+    assert lib.delta_decode_step(P(s), 3, roles, kvs, ptrs, ptrs, P(sel), None, fake, fake, need, None) == -1
+    roles_bad = (ctypes.c_int32 * 3)(0, 3, 2)
+    assert lib.delta_decode_step(P(s), 3, roles_bad, kvs, ptrs, ptrs, P(sel), fake, fake, fake, need, None) == -1
+    nullq = (ctypes.c_void_p * 3)(0x1000, None, 0x1000)
+    assert lib.delta_decode_step(P(s), 3, roles, kvs, nullq, ptrs, P(sel), fake, fake, fake, need, None) == -1
