@@ -145,7 +145,7 @@ def test_duplicated_pages_force_exact_ties():
     top = int(np.argmax(S0[:-w.recent_units]))
     pt = inp.page_table.clone()
     dups = [u for u in range(1, 60) if u != top][:48]
-    pt[0, dups] = pt[0, top]        # 48 exact copies of the best page among the candidates
+    pt[0, dups] = int(pt[0, top])   # 48 exact copies of the best page among the candidates
     inp.page_table = pt
     res = run_step(inp)
     q, K, V = oracle_kv(inp, 1, 0, host_cache_of(inp, 1))
