@@ -88,11 +88,54 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   const int Hq = a.n_q_heads;
   const int bg = b * a.n_kv_heads + g;
 
+  // ---- start-up: the query operand, the sequence length / selection count and this split's
+  // page (or row) list are all requested at once; the list is staged in LDS speculatively
+  // (bounded by the host's group bound) and trimmed once the length is known.
+  bf16x8 qb[Gm::NK];
+  {
+    const uint16_t* qp = a.q + ((size_t)b * Hq + g * G + min(hcol, G - 1)) * D + 8 * quad;
+#pragma unroll
+    for (int ks = 0; ks < Gm::NK; ++ks) {
+      u32x4 w = load16(qp + 32 * ks);
+      if (hcol >= G) w = u32x4{0u, 0u, 0u, 0u};
+      qb[ks] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
   const int s_b = a.seq_lens[b];
+  const int sel_n = (MODE == ROWS_DENSE) ? 0 : min(a.sel_cnt[b], a.sel_stride);
+  const int g0 = split * a.gps;
+  const int cand = max(0, min(a.gps, a.max_groups - g0));
+
+  __shared__ int s_rows[kMaxRowSlots];
+  __shared__ int s_aux[kMaxRowSlots];
+  const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
+  if (MODE == ROWS_DENSE) {
+    for (int i = tid; i < cand; i += kAttnThreads) s_rows[i] = pt[g0 + i];
+  } else if (MODE == ROWS_SEL_PAGE) {
+    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    for (int i = tid; i < cand; i += kAttnThreads) {
+      const int u = sel[g0 + i];
+      const bool ok = u >= 0 && u < a.max_pages;
+      s_rows[i] = ok ? pt[u] : 0;
+      s_aux[i] = ok ? u : 0;
+    }
+  } else {
+    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    const int n_rows = min(16 * cand, a.sel_stride - 16 * g0);
+    for (int i = tid; i < 16 * cand; i += kAttnThreads) {
+      int packed = -1;
+      if (i < n_rows) {
+        const int t = sel[16 * g0 + i];
+        if (t >= 0 && t < 16 * a.max_pages) packed = pt[t >> 4] * 16 + (t & 15);
+      }
+      s_rows[i] = packed;
+    }
+  }
+
   int n_groups;
   if (MODE == ROWS_DENSE) n_groups = (s_b + 15) >> 4;
-  else if (MODE == ROWS_SEL_PAGE) n_groups = a.sel_cnt[b];
-  else n_groups = (a.sel_cnt[b] + 15) >> 4;
+  else if (MODE == ROWS_SEL_PAGE) n_groups = sel_n;
+  else n_groups = (sel_n + 15) >> 4;
   // lengths beyond the host bound are clamped so that no access leaves the buffers
   n_groups = max(0, min(n_groups, a.max_groups));
   const int n_valid = (n_groups + a.gps - 1) / a.gps;
@@ -106,79 +149,36 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     return;
   }
   if (split >= n_valid) return;
-
-  const int g0 = split * a.gps;
   const int ng = min(a.gps, n_groups - g0);
-
-  // ---- stage this split's page (or row) list in LDS -----------------------------------
-  __shared__ int s_rows[kMaxRowSlots];
-  __shared__ int s_aux[kMaxRowSlots];
-  const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
-  if (MODE == ROWS_DENSE) {
-    for (int i = tid; i < ng; i += kAttnThreads) {
-      s_rows[i] = pt[g0 + i];
-      s_aux[i] = min(16, s_b - 16 * (g0 + i));
-    }
-  } else if (MODE == ROWS_SEL_PAGE) {
-    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
-    for (int i = tid; i < ng; i += kAttnThreads) {
-      const int u = sel[g0 + i];
-      s_rows[i] = pt[u];
-      s_aux[i] = min(16, s_b - 16 * u);
-    }
-  } else {
-    const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
-    const int cnt = min(a.sel_cnt[b], a.sel_stride);
-    for (int i = tid; i < 16 * ng; i += kAttnThreads) {
-      const int idx = 16 * g0 + i;
-      int packed = -1;
-      if (idx < cnt) {
-        const int t = sel[idx];
-        packed = pt[t >> 4] * 16 + (t & 15);
-      }
-      s_rows[i] = packed;
-    }
-  }
   __syncthreads();
-
-  // ---- query operand (MFMA B: k = head dim, n = query head, zero-padded to 16) -----------
-  bf16x8 qb[Gm::NK];
-  {
-    const uint16_t* qp = a.q + ((size_t)b * Hq + g * G + min(hcol, G - 1)) * D + 8 * quad;
-#pragma unroll
-    for (int ks = 0; ks < Gm::NK; ++ks) {
-      u32x4 w = load16(qp + 32 * ks);
-      if (hcol >= G) w = u32x4{0u, 0u, 0u, 0u};
-      qb[ks] = __builtin_bit_cast(bf16x8, w);
-    }
-  }
 
   const size_t head_off = (size_t)g * 16 * D;
   auto load_tile = [&](Tile<D>& t, int li) {
     if (MODE == ROWS_SEL_TOKEN) {
-      // every row is its own (page, row); invalid rows re-read the group's first row
+      // every row is its own (page, row); rows past the selection re-read the group's first
       const int* rows = s_rows + 16 * li;
+      const int base = 16 * (g0 + li);
       const int first = rows[0];
-      int kr = rows[hcol];
       t.kmask = 0;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) t.kmask |= (rows[r] >= 0 ? 1u : 0u) << r;
-      if (kr < 0) kr = first;
+      for (int r = 0; r < 16; ++r) t.kmask |= ((rows[r] >= 0 && base + r < sel_n) ? 1u : 0u) << r;
+      int kr = ((t.kmask >> hcol) & 1u) ? rows[hcol] : first;
       const uint16_t* kp = a.k_cache + (size_t)(kr >> 4) * a.page_stride + head_off +
                            (size_t)(kr & 15) * D + 8 * quad;
 #pragma unroll
       for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
 #pragma unroll
       for (int i = 0; i < Gm::NI; ++i) {
-        int vr = rows[Gm::RPI * i + lane / Gm::LPR];
-        if (vr < 0) vr = first;
+        const int r = Gm::RPI * i + lane / Gm::LPR;
+        const int vr = ((t.kmask >> r) & 1u) ? rows[r] : first;
         t.v[i] = load16(a.v_cache + (size_t)(vr >> 4) * a.page_stride + head_off +
                         (size_t)(vr & 15) * D + 8 * (lane % Gm::LPR));
       }
     } else {
       const size_t page = (size_t)s_rows[li] * a.page_stride + head_off;
-      const int nrows = s_aux[li];
-      t.kmask = (nrows >= 16) ? 0xffffu : ((1u << nrows) - 1u);
+      const int unit = (MODE == ROWS_DENSE) ? g0 + li : s_aux[li];
+      const int nrows = min(16, s_b - 16 * unit);
+      t.kmask = (nrows >= 16) ? 0xffffu : ((1u << max(nrows, 0)) - 1u);
       const uint16_t* kp = a.k_cache + page + (size_t)hcol * D + 8 * quad;
 #pragma unroll
       for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
@@ -217,12 +217,15 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);          // finite: row 0 of a group always exists
-    const float alpha = exp2f(m_run - m_new);
+    const float m_new = fmaxf(m_run, mx);
+    // m_new is finite whenever the group has a valid row (always, for valid selections); the
+    // guard keeps an all-masked group from turning the running state into NaN
+    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+    const float alpha = exp2f(m_run - m_use);
     float p[4], ps = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      p[r] = exp2f(x[r] - m_new);
+      p[r] = exp2f(x[r] - m_use);
       ps += p[r];
     }
     ps += __shfl_xor(ps, 16);
@@ -265,13 +268,28 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     }
   };
 
+  // Each wave walks groups wave, wave+4, ... through a ring of three register tiles, so two
+  // groups' loads are in flight while one is consumed.  Loads past the wave's last group are
+  // clamped to that group (already requested by this wave: served by the caches).
   if (wave < ng) {
-    Tile<D> cur, nxt;
-    load_tile(cur, wave);
-    for (int li = wave; li < ng; li += kWaves) {
-      load_tile(nxt, min(li + kWaves, ng - 1));   // clamped prefetch keeps loads unconditional
-      process(cur, li);
-      cur = nxt;
+    const int last = wave + ((ng - 1 - wave) / kWaves) * kWaves;
+    Tile<D> t0, t1, t2;
+    int li = wave;
+    load_tile(t0, li);
+    load_tile(t1, min(li + kWaves, last));
+    while (true) {
+      load_tile(t2, min(li + 2 * kWaves, last));
+      process(t0, li);
+      li += kWaves;
+      if (li >= ng) break;
+      load_tile(t0, min(li + 2 * kWaves, last));
+      process(t1, li);
+      li += kWaves;
+      if (li >= ng) break;
+      load_tile(t1, min(li + 2 * kWaves, last));
+      process(t2, li);
+      li += kWaves;
+      if (li >= ng) break;
     }
   }
 
@@ -319,13 +337,22 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   }
 
   // ---- last workgroup of (b, g) merges the splits -----------------------------------------
-  __threadfence();
+  // Every thread waits for its partial stores to complete; after the barrier one thread
+  // publishes the workgroup's partial with a device-scope release and counts it in.  The
+  // workgroup that brings the count to n_valid acquires (device scope) before reading the
+  // other workgroups' partials.  One release per workgroup keeps the cache write-back cost low.
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   __shared__ int s_last;
-  if (tid == 0) s_last = (atomicAdd(&a.counters[bg], 1) == n_valid - 1);
+  if (tid == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    const int prev = __hip_atomic_fetch_add(&a.counters[bg], 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = prev == n_valid - 1;
+    if (s_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
 
   __shared__ float s_f[kMaxSplits][kMaxGroup];   // per split and head: exp2(m_c - M)
   __shared__ float s_sl[kMaxSplits][kMaxGroup];  // per split and head: l_c

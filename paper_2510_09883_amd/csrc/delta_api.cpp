@@ -22,13 +22,15 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Workgroups the attention launch aims for: several per CU on 256 CUs, so that the chip fills
-// and the ragged tail of one launch is short.  DELTA_ATTN_TARGET_WGS overrides it for tuning.
+// Workgroups the attention launch aims for: about one per CU (256 CUs).  Fewer, longer
+// workgroups keep the number of device-scope releases of the split combine low (each one
+// writes back the XCD's L2), which measured faster than more, shorter workgroups at every
+// workload size.  DELTA_ATTN_TARGET_WGS overrides it for tuning.
 int target_workgroups() {
   static int v = [] {
     const char* e = getenv("DELTA_ATTN_TARGET_WGS");
     int x = e ? atoi(e) : 0;
-    return x > 0 ? x : 1024;
+    return x > 0 ? x : 256;
   }();
   return v;
 }
@@ -228,6 +230,8 @@ int run_sparse(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void
 
 }  // namespace
 
+// Only the C ABI is exported; everything else in the library has hidden visibility.
+#pragma GCC visibility push(default)
 extern "C" {
 
 int delta_workspace_bytes(const delta_shape_t* shape, const delta_select_t* sel, size_t* out) {
@@ -339,3 +343,4 @@ const char* delta_status_string(int status) {
 }
 
 }  // extern "C"
+#pragma GCC visibility pop

@@ -46,20 +46,30 @@ class delta_select_t(ctypes.Structure):
 
 _P = ctypes.POINTER
 _vp = ctypes.c_void_p
-_lib.delta_workspace_bytes.argtypes = [_P(delta_shape_t), _P(delta_select_t), _P(ctypes.c_size_t)]
-_lib.delta_workspace_init.argtypes = [_vp, ctypes.c_size_t, _vp]
-_lib.delta_full_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _vp, ctypes.c_size_t, _vp]
-_lib.delta_delta_attn_select.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp,
-                                         _P(delta_select_t), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
-_lib.delta_sparse_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _P(delta_select_t),
-                                   _vp, _vp, _vp, ctypes.c_size_t, _vp]
-_lib.delta_decode_step.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
-                                   _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
-                                   _vp, _vp, _vp, ctypes.c_size_t, _vp]
-_lib.delta_status_string.argtypes = [ctypes.c_int]
-_lib.delta_status_string.restype = ctypes.c_char_p
-for _n in EXPORTED[:-1]:
-    getattr(_lib, _n).restype = ctypes.c_int
+
+
+def _bind(lib):
+    """Declare the C signatures of include/delta_attn.h on a loaded library handle."""
+    lib.delta_workspace_bytes.argtypes = [_P(delta_shape_t), _P(delta_select_t), _P(ctypes.c_size_t)]
+    lib.delta_workspace_init.argtypes = [_vp, ctypes.c_size_t, _vp]
+    lib.delta_full_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.delta_delta_attn_select.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp,
+                                            _P(delta_select_t), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.delta_sparse_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _P(delta_select_t),
+                                      _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.delta_decode_step.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
+                                      _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
+                                      _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.delta_hbm_read_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, ctypes.c_int32, _vp]
+    lib.delta_hbm_read_probe.restype = ctypes.c_int
+    lib.delta_status_string.argtypes = [ctypes.c_int]
+    lib.delta_status_string.restype = ctypes.c_char_p
+    for n in EXPORTED[:-1]:
+        getattr(lib, n).restype = ctypes.c_int
+    return lib
+
+
+_lib = _bind(_lib)
 
 
 class DeltaError(RuntimeError):
@@ -162,3 +172,10 @@ def delta_decode_step(args: StepArgs):
                                   ctypes.byref(a.sel) if a.sel is not None else None,
                                   _ptr(a.sel_idx), _ptr(a.sel_cnt), _ptr(a.ws), _nbytes(a.ws),
                                   _stream()))
+
+
+def delta_hbm_read_probe(buf, sink, n_workgroups=2048, unroll=4):
+    """Streaming read of `buf` (include/delta_probe.h); sink: int32/uint32 [n_workgroups]."""
+    rc = _lib.delta_hbm_read_probe(_ptr(buf), _nbytes(buf), _ptr(sink), n_workgroups, unroll, _stream())
+    if rc != 0:
+        raise DeltaError("delta_hbm_read_probe", rc)

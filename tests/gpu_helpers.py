@@ -56,7 +56,7 @@ def run_step(inp, roles=None, agg=0, budget=None, recent=None, ws=None):
     sel_cnt = torch.full((n_delta, w.batch), -7, dtype=torch.int32, device="cuda")
     kvs = [d.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
            for i in range(len(roles))]
-    args = d.StepArgs(shape, roles, kvs, inp.q, outs, sel, sel_idx, sel_cnt, ws)
+    args = d.StepArgs(shape, roles, kvs, inp.q[:len(roles)], outs, sel, sel_idx, sel_cnt, ws)
     d.delta_decode_step(args)
     torch.cuda.synchronize()
     return StepResult(outs, sel_idx, sel_cnt)

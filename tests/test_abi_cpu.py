@@ -8,6 +8,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "delta_attn.h")
+PROBE_HEADER = os.path.join(ROOT, "include", "delta_probe.h")
 
 
 @pytest.fixture(scope="module")
@@ -16,8 +17,8 @@ def D():
     return delta
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(path=HEADER):
+    text = open(path).read()
     return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(delta_\w+)\s*\(", text, re.M)))
 
 
@@ -28,6 +29,16 @@ def test_library_exports_every_declared_symbol(D):
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(D.EXPORTED) == names
+    probe = declared_functions(PROBE_HEADER)
+    assert probe == ["delta_hbm_read_probe"] and hasattr(lib, probe[0])
+
+
+def test_probe_rejects_bad_arguments(D):
+    lib = D._lib
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.delta_hbm_read_probe(None, 1 << 20, fake, 64, 4, None) == -1
+    assert lib.delta_hbm_read_probe(fake, 1 << 20, fake, 64, 3, None) == -1
+    assert lib.delta_hbm_read_probe(ctypes.c_void_p(0x1001), 1 << 20, fake, 64, 4, None) == -1
 
 
 def test_status_strings(D):

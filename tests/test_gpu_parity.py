@@ -238,3 +238,22 @@ def test_full_size_sampled(cfg, seqs):
             assert set(range(n_u - w.recent_units, n_u)) <= set(r.tolist())
     del inp, res
     torch.cuda.empty_cache()
+
+
+def test_shared_workspace_alternating_inputs():
+    """Calls on one workspace with different inputs: every call must see only its own split
+    partials (no stale data from the previous call), on every layer."""
+    d = D()
+    w = configs.get(2)
+    w.batch = 2
+    a = synth.make_inputs(w, "cuda", seq_lens=[8192, 5000], layers=range(4))
+    w2 = configs.get(2)
+    w2.batch, w2.cfg_id = 2, 7
+    b = synth.make_inputs(w2, "cuda", seq_lens=[8192, 5000], layers=range(4))
+    roles = [ROLE_FULL, ROLE_DELTA, ROLE_SPARSE, ROLE_SPARSE]
+    shape, sel = shape_of(a), select_of(w)
+    ws = d.alloc_workspace(shape, sel)
+    for rep in range(2):
+        for inp in (a, b):
+            res = run_step(inp, roles=roles, ws=ws)
+            check_step(inp, res, roles=roles).assert_ok()
