@@ -223,6 +223,27 @@ def cpu_baseline(w, inp, roles, budget_s):
             "sample": sample, "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def measured_traffic(role, w, kernel_tag):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a known-size copy), or None when there is none for this
+    kernel and workload or the kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_{role}_{w.name}.md")
+    src = os.path.join(ROOT, "paper_2510_09883_amd", "csrc", "attn_kernel.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel") != kernel_tag:
+        return None
+    if kv.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
 def copy_calibration():
     """A plain device copy of known size (64 MiB read + 64 MiB written), for scaling the
     FETCH_SIZE / WRITE_SIZE counters of the profiled kernels."""
@@ -298,6 +319,9 @@ def main():
     dominant = max(layer_us, key=lambda r: layer_us[r] * per_step[r])
     kernel_name = {"full": "attn_kernel (dense rows)", "delta": "attn_kernel + score + select",
                    "sparse": "attn_kernel (selected pages)"}[dominant]
+    mode = {"full": 0, "delta": 0, "sparse": 1 if w.unit_tokens == 16 else 2}[dominant]
+    kernel_tag = f"attn_kernel<{w.head_dim}, {w.group}, {mode}>"
+    traffic = measured_traffic(dominant, w, kernel_tag)
     achieved = role_bytes[dominant] / (layer_us[dominant] * 1e-6) / 1e9
     overhead = (layer_us["delta"] - layer_us["full"]) / layer_us["full"] if "delta" in layer_us and "full" in layer_us else None
 
@@ -344,7 +368,7 @@ def main():
         "delta_select_overhead": None if overhead is None else round(overhead, 4),
         "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "bytes_per_launch": int(role_bytes[dominant]),
+                     "traffic": traffic, "bytes_per_launch": int(role_bytes[dominant]),
                      "avg_launch_us": round(layer_us[dominant], 3)},
         "cpu_baseline": cpu,
     }

@@ -3,7 +3,8 @@
 // What it computes (Sec. 2, Eq. gqa_attention; App. A, Alg. 1): for sequence b and query
 // head j, out = sum_t softmax_t(scale * q_j . k_t) v_t over the rows of the sequence that the
 // mode selects, with k_t, v_t read from KV head j / G.  In Delta mode the scaled logits of
-// every token and the per-head log-sum-exp are also written, for the page scoring of
+// every token (page-major: [b][page][head][row]) and the per-head log-sum-exp are also
+// written, for the page scoring of
 // Sec. 4 ("Selection mechanism", "Page-based DELTA").
 //
 // Work decomposition.  One workgroup (4 waves) per (split, kv head g, sequence b).  A split
@@ -211,7 +212,9 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     for (int r = 0; r < 4; ++r)
       x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
     if (MODE == ROWS_DENSE && a.logits != nullptr && hcol < G) {
-      float* lg = a.logits + (size_t)(Hq_row + hcol) * a.logit_stride + 16 * (g0 + li) + 4 * quad;
+      // page-major [b][page][head][16]: the G heads of this KV group are adjacent, so one
+      // store writes G*64 contiguous bytes (whole cache lines)
+      float* lg = a.logits + (((size_t)b * a.logit_pages + (g0 + li)) * Hq + g * G + hcol) * 16 + 4 * quad;
       *reinterpret_cast<f32x4*>(lg) = f32x4{x[0], x[1], x[2], x[3]};
     }
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));

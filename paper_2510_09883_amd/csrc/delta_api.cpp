@@ -72,7 +72,7 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
 struct Layout {
   size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, total = 0;
   int max_split = 0;
-  int logit_stride = 0;
+  int logit_pages = 0;
   int nu_stride = 0;
   SplitPlan dense, sparse;
   int sparse_mode = ROWS_SEL_PAGE;
@@ -126,14 +126,14 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     }
     L->max_split = std::max(L->max_split, L->sparse.n_split);
   }
-  L->logit_stride = ceil_div(s->max_seq_len, 16) * 16;
+  L->logit_pages = ceil_div(s->max_seq_len, 16);
   size_t off = 0;
   L->counters = off;  off = align_up(off + sizeof(int32_t) * pairs);
   L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * 2);
   L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * s->head_dim);
   if (sel) {
     L->nu_stride = ceil_div(s->max_seq_len, sel->unit_tokens);
-    L->logits = off;  off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads * L->logit_stride);
+    L->logits = off;  off = align_up(off + sizeof(float) * (size_t)s->batch * L->logit_pages * s->n_q_heads * 16);
     L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
     L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
   }
@@ -168,7 +168,7 @@ AttnArgs base_args(const delta_shape_t* s, const delta_kv_t* kv, const void* q, 
   a.n_q_heads = s->n_q_heads;
   a.n_kv_heads = s->n_kv_heads;
   a.max_pages = s->max_pages_per_seq;
-  a.logit_stride = L.logit_stride;
+  a.logit_pages = L.logit_pages;
   a.n_split = plan.n_split;
   a.gps = plan.gps;
   a.max_groups = plan.max_groups;
@@ -200,7 +200,7 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   sa.seq_lens = kv->seq_lens;
   sa.unit_scores = uscores ? uscores : reinterpret_cast<float*>(ws + L.uscores);
   sa.n_q_heads = s->n_q_heads;
-  sa.logit_stride = L.logit_stride;
+  sa.logit_pages = L.logit_pages;
   sa.nu_stride = L.nu_stride;
   sa.max_seq_len = s->max_seq_len;
   rc = hip_rc(launch_score(sel->agg, sel->unit_tokens, sa, s->batch, st));

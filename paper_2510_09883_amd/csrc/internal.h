@@ -31,10 +31,10 @@ struct AttnArgs {
   float* part_o;             // [B*Hkv, n_split, G, D]   un-normalised split outputs
   float* part_ml;            // [B*Hkv, n_split, G, 2]   split (max, sum) in the log2 domain
   int32_t* counters;         // [B*Hkv] arrival counters, zero between launches
-  float* logits;             // [B, Hq, logit_stride] log2-domain logits, or null
+  float* logits;             // [B, logit_pages, Hq, 16] log2-domain logits, or null
   float* lse;                // [B, Hq] log2-domain log-sum-exp, or null
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
-  int32_t n_q_heads, n_kv_heads, max_pages, sel_stride, logit_stride;
+  int32_t n_q_heads, n_kv_heads, max_pages, sel_stride, logit_pages;
   int32_t n_split, gps;      // splits per (b, kv head) and 16-row groups per split
   int32_t max_groups;        // host bound on groups per sequence (n_split * gps >= it)
   float scale_log2;          // sm_scale * log2(e)
@@ -44,11 +44,11 @@ hipError_t launch_attention(int head_dim, int group, int mode, const AttnArgs& a
                             hipStream_t stream);
 
 struct ScoreArgs {
-  const float* logits;       // [B, Hq, logit_stride]
+  const float* logits;       // [B, logit_pages, Hq, 16]
   const float* lse;          // [B, Hq]
   const int32_t* seq_lens;   // [B]
   float* unit_scores;        // [B, nu_stride]
-  int32_t n_q_heads, logit_stride, nu_stride, max_seq_len;
+  int32_t n_q_heads, logit_pages, nu_stride, max_seq_len;
 };
 
 hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,
