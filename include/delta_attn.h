@@ -82,7 +82,9 @@ typedef struct {
 
 /* Selection parameters (Sec. 4; App. A, Alg. 2).  All counts are in TOKENS and must be whole
  * units: budget k = K*U, recency window l = L*U.  unit_tokens U = 16 is page-based DELTA (the
- * paper's configuration); U = 1 is the token-level rule of Sec. 4. */
+ * paper's configuration); U = 1 is the token-level rule of Sec. 4.  A sequence may have at most
+ * 8192 candidate units (units older than the recency window): 131072 tokens with pages, about
+ * 8192 with single tokens; larger shapes return DELTA_ERR_UNSUPPORTED. */
 typedef struct {
   int32_t budget_tokens;      /* k: tokens kept per sequence, a multiple of U, > recent       */
   int32_t recent_tokens;      /* l: most recent tokens always kept, a multiple of U, >= 0     */

@@ -3,8 +3,8 @@
 // What it computes (Sec. 2, Eq. gqa_attention; App. A, Alg. 1): for sequence b and query
 // head j, out = sum_t softmax_t(scale * q_j . k_t) v_t over the rows of the sequence that the
 // mode selects, with k_t, v_t read from KV head j / G.  In Delta mode the scaled logits of
-// every token (page-major: [b][page][head][row]) and the per-head log-sum-exp are also
-// written, for the page scoring of
+// every token (group-major: [b][kv group][page][head in group][row]) and the per-head
+// log-sum-exp are also written, for the page scoring of
 // Sec. 4 ("Selection mechanism", "Page-based DELTA").
 //
 // Work decomposition.  One workgroup (4 waves) per (split, kv head g, sequence b).  A split
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   const int b = blockIdx.z;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int quad = lane >> 4;   // score-tile rows 4*quad .. 4*quad+3
   const int hcol = lane & 15;   // score-tile column = query head within the group
   const int Hq = a.n_q_heads;
@@ -212,9 +212,9 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     for (int r = 0; r < 4; ++r)
       x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
     if (MODE == ROWS_DENSE && a.logits != nullptr && hcol < G) {
-      // page-major [b][page][head][16]: the G heads of this KV group are adjacent, so one
-      // store writes G*64 contiguous bytes (whole cache lines)
-      float* lg = a.logits + (((size_t)b * a.logit_pages + (g0 + li)) * Hq + g * G + hcol) * 16 + 4 * quad;
+      // group-major [b][g][page][G][16]: a workgroup's logits form one contiguous stream
+      // (pages g0 .. g0+gps of its KV group), written G*64 bytes per group
+      float* lg = a.logits + ((((size_t)b * a.n_kv_heads + g) * a.logit_pages + (g0 + li)) * G + hcol) * 16 + 4 * quad;
       *reinterpret_cast<f32x4*>(lg) = f32x4{x[0], x[1], x[2], x[3]};
     }
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));

@@ -125,6 +125,9 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
         return DELTA_ERR_UNSUPPORTED;
     }
     L->max_split = std::max(L->max_split, L->sparse.n_split);
+    // the selection holds the older units of one sequence in one workgroup's registers
+    if (ceil_div(s->max_seq_len, sel->unit_tokens) - sel->recent_tokens / sel->unit_tokens > kMaxSelectKeys)
+      return DELTA_ERR_UNSUPPORTED;
   }
   L->logit_pages = ceil_div(s->max_seq_len, 16);
   size_t off = 0;
@@ -200,6 +203,7 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   sa.seq_lens = kv->seq_lens;
   sa.unit_scores = uscores ? uscores : reinterpret_cast<float*>(ws + L.uscores);
   sa.n_q_heads = s->n_q_heads;
+  sa.n_kv_heads = s->n_kv_heads;
   sa.logit_pages = L.logit_pages;
   sa.nu_stride = L.nu_stride;
   sa.max_seq_len = s->max_seq_len;

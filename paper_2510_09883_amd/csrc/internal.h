@@ -18,6 +18,7 @@ constexpr int kAttnThreads = 256;        // 4 waves of 64
 constexpr int kMaxSplits = 64;           // split partials combined by the last workgroup
 constexpr int kMaxRowSlots = 1024;       // LDS slots staging a split's page / row list
 constexpr int kMaxGroup = 8;             // query heads per KV head (padded to 16 MFMA columns)
+constexpr int kMaxSelectKeys = 8192;     // candidate units one selection workgroup holds in registers
 
 struct AttnArgs {
   const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
@@ -31,7 +32,7 @@ struct AttnArgs {
   float* part_o;             // [B*Hkv, n_split, G, D]   un-normalised split outputs
   float* part_ml;            // [B*Hkv, n_split, G, 2]   split (max, sum) in the log2 domain
   int32_t* counters;         // [B*Hkv] arrival counters, zero between launches
-  float* logits;             // [B, logit_pages, Hq, 16] log2-domain logits, or null
+  float* logits;             // [B, Hkv, logit_pages, G, 16] log2-domain logits, or null
   float* lse;                // [B, Hq] log2-domain log-sum-exp, or null
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
   int32_t n_q_heads, n_kv_heads, max_pages, sel_stride, logit_pages;
@@ -44,11 +45,11 @@ hipError_t launch_attention(int head_dim, int group, int mode, const AttnArgs& a
                             hipStream_t stream);
 
 struct ScoreArgs {
-  const float* logits;       // [B, logit_pages, Hq, 16]
+  const float* logits;       // [B, Hkv, logit_pages, G, 16]
   const float* lse;          // [B, Hq]
   const int32_t* seq_lens;   // [B]
   float* unit_scores;        // [B, nu_stride]
-  int32_t n_q_heads, logit_pages, nu_stride, max_seq_len;
+  int32_t n_q_heads, n_kv_heads, logit_pages, nu_stride, max_seq_len;
 };
 
 hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,

@@ -8,12 +8,14 @@
 //   S_u = sum of s_t over the unit's tokens: a 16-lane butterfly for pages, the token itself
 //   for token-level units.
 //
-// select_kernel: one wave per sequence (no workgroup barriers).  Units [n_u - L, n_u) are kept; among
+// select_kernel: one 256-thread workgroup per sequence, candidate keys in registers.  Units
+//   [n_u - L, n_u) are kept; among
 //   the n_u - L older units the (K - L) largest scores are found by an exact radix select on
-//   the float bit patterns (non-negative floats order like their uint32 bits): four 8-bit
-//   digit histograms in LDS give the exact threshold key T and how many keys equal to T are
-//   needed.  A final pass in index order takes every key > T and the lowest-index keys == T
-//   (ballot prefix counts), writing them in ascending order.  While n_u <= K every unit is
+//   the float bit patterns (non-negative floats order like their uint32 bits): after skipping
+//   the leading bits common to all keys, 8-bit digit histograms in LDS give the exact
+//   threshold key T and how many keys equal to T are needed.  A final pass in index order
+//   takes every key > T and the lowest-index keys == T (block prefix sums), writing them in
+//   ascending order.  While n_u <= K every unit is
 //   kept.
 #include "internal.h"
 
@@ -22,8 +24,9 @@ namespace {
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kScoreThreads = 256;
-constexpr int kSelectThreads = 64;   // one wave per sequence
-constexpr int kLdsKeys = 8192;   // candidate keys cached in LDS when they fit
+constexpr int kSelectThreads = 256;
+constexpr int kSelectWaves = kSelectThreads / 64;
+constexpr int kKeysPerThread = kMaxSelectKeys / kSelectThreads;
 
 template <int AGG, int U>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a) {
@@ -35,16 +38,25 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
   const float* lse = a.lse + (size_t)b * Hq;
   float sc = 0.f;
   if (t < s_b) {
-    // page-major logits [b][page][head][16]: token t is row t%16 of page t/16
-    const float* row = a.logits + ((size_t)b * a.logit_pages + (t >> 4)) * Hq * 16 + (t & 15);
+    // group-major logits [b][g][page][h][16]: token t is row t%16 of page t/16; head j = g*G + h
+    const int G = Hq / a.n_kv_heads;
+    const size_t gstride = (size_t)a.logit_pages * G * 16;
+    const float* row = a.logits + (size_t)b * a.n_kv_heads * gstride + (size_t)(t >> 4) * G * 16 + (t & 15);
+    // one flat loop over all heads (j = g*G + h) so that eight loads are in flight at a time
     if (AGG == 0) {
       float m = kNegInf;
 #pragma unroll 8
-      for (int j = 0; j < Hq; ++j) m = fmaxf(m, row[j * 16] - lse[j]);
+      for (int j = 0; j < Hq; ++j) {
+        const int g = j / G, h = j - g * G;
+        m = fmaxf(m, row[g * gstride + h * 16] - lse[j]);
+      }
       sc = exp2f(m);
     } else {
 #pragma unroll 8
-      for (int j = 0; j < Hq; ++j) sc += exp2f(row[j * 16] - lse[j]);
+      for (int j = 0; j < Hq; ++j) {
+        const int g = j / G, h = j - g * G;
+        sc += exp2f(row[g * gstride + h * 16] - lse[j]);
+      }
     }
   }
   float* out = a.unit_scores + (size_t)b * a.nu_stride;
@@ -63,18 +75,36 @@ __device__ __forceinline__ uint32_t key_of(float f) {
   return f > 0.f ? __float_as_uint(f) : 0u;   // scores are >= 0; NaN / -0 map to 0
 }
 
-// Wave-synchronous LDS ordering (one wave's LDS requests execute in order; this keeps the
-// compiler from moving them).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+// Exclusive prefix sum of one int per thread over the workgroup; *total gets the sum.
+__device__ __forceinline__ int block_excl_scan(int v, int* s_wave, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) s_wave[w] = incl;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kSelectWaves; ++i) {
+    const int c = s_wave[i];
+    base += (i < w) ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + incl - v;
 }
 
-// One wave per sequence: no workgroup barriers anywhere.
+// One workgroup per sequence.  Thread t owns the candidate keys [t*kpt, t*kpt + kpt) in
+// registers (kpt <= kKeysPerThread), so index order is thread order then slot order and one
+// block scan places every chosen unit.
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs a) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
   const int U = a.unit_tokens;
   const int K = a.budget_units;
   const int L = a.recent_units;
@@ -83,98 +113,135 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
   int32_t* idx_out = a.sel_idx + (size_t)b * K;
 
   if (n_u <= K) {   // the context fits the budget: keep every unit
-    for (int i = lane; i < K; i += kSelectThreads) idx_out[i] = (i < n_u) ? i : -1;
-    if (lane == 0) a.sel_cnt[b] = max(n_u, 0);
+    for (int i = tid; i < K; i += kSelectThreads) idx_out[i] = (i < n_u) ? i : -1;
+    if (tid == 0) a.sel_cnt[b] = max(n_u, 0);
     return;
   }
-  const int n_c = n_u - L;      // candidate (older) units
+  const int n_c = min(n_u - L, kMaxSelectKeys);   // candidate (older) units; the host bounds it
   const int need = K - L;       // >= 1
   const float* S = a.unit_scores + (size_t)b * a.nu_stride;
-  const unsigned long long lt_mask = (1ull << lane) - 1ull;
+  const int kpt = (n_c + kSelectThreads - 1) / kSelectThreads;
+  const int i0 = tid * kpt;
 
-  __shared__ uint32_t s_keys[kLdsKeys];
   __shared__ uint32_t s_hist[256];
-  const bool in_lds = n_c <= kLdsKeys;
-  if (in_lds) {
-    // eight independent loads in flight per lane before any is stored
-    for (int i0 = 0; i0 < n_c; i0 += 8 * kSelectThreads) {
-      float v[8];
+  __shared__ int s_wave[kSelectWaves];
+  __shared__ uint32_t s_red[2][kSelectWaves];
+  __shared__ int s_digit, s_above;
+
+  uint32_t key[kKeysPerThread];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * kSelectThreads + lane;
-        v[u] = (i < n_c) ? S[i] : 0.f;
-      }
+  for (int j = 0; j < kKeysPerThread; ++j) {
+    const int i = i0 + j;
+    key[j] = (j < kpt && i < n_c) ? key_of(S[i]) : 0u;
+  }
+  // Bits shared by every candidate key need no histogram: start the digit passes at the
+  // highest bit where two keys differ (page scores mostly share sign and high exponent bits,
+  // which would otherwise send every key of the first pass to the same bin).
+  uint32_t k_or = 0u, k_and = 0xffffffffu;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * kSelectThreads + lane;
-        if (i < n_c) s_keys[i] = key_of(v[u]);
-      }
+  for (int j = 0; j < kKeysPerThread; ++j) {
+    if (j < kpt && i0 + j < n_c) {
+      k_or |= key[j];
+      k_and &= key[j];
     }
   }
-  auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : key_of(S[i]); };
-
-  uint32_t prefix = 0;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    k_or |= (uint32_t)__shfl_xor((int)k_or, off);
+    k_and &= (uint32_t)__shfl_xor((int)k_and, off);
+  }
+  if (lane == 0) {
+    s_red[0][tid >> 6] = k_or;
+    s_red[1][tid >> 6] = k_and;
+  }
+  __syncthreads();
+  k_or = 0u;
+  k_and = 0xffffffffu;
+#pragma unroll
+  for (int w = 0; w < kSelectWaves; ++w) {
+    k_or |= s_red[0][w];
+    k_and &= s_red[1][w];
+  }
+  const uint32_t differ = k_or ^ k_and;
+  int low = differ ? 32 - __clz((int)differ) : 0;   // bits [low, 32) are common to all keys
+  uint32_t prefix = low >= 32 ? 0u : (k_and & ~((1u << low) - 1u));
   int remaining = need;   // rank of the threshold among the keys matching `prefix`
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = lane; i < 256; i += kSelectThreads) s_hist[i] = 0;
-    wave_lds_sync();
-    for (int i = lane; i < n_c; i += kSelectThreads) {
-      const uint32_t k = key_at(i);
-      const bool match = (pass == 0) || ((k >> (shift + 8)) == (prefix >> (shift + 8)));
-      if (match) atomicAdd(&s_hist[(k >> shift) & 255u], 1u);
-    }
-    wave_lds_sync();
-    // lane l owns digits 255-4l .. 252-4l (descending); the lane where the running count
-    // from the top reaches `remaining` holds the threshold's digit
-    int c[4], sum = 0;
+  while (low > 0) {
+    const int width = min(8, low);
+    const int shift = low - width;
+    const int top = shift + width;                    // bits [top, 32) already fixed
+    s_hist[tid] = 0u;                                 // kSelectThreads == 256 bins
+    __syncthreads();
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      c[k] = (int)s_hist[255 - 4 * lane - k];
-      sum += c[k];
+    for (int j = 0; j < kKeysPerThread; ++j) {
+      const uint32_t k = key[j];
+      const bool match = j < kpt && i0 + j < n_c && (top >= 32 || (k >> top) == (prefix >> top));
+      if (match) atomicAdd(&s_hist[(k >> shift) & ((1u << width) - 1u)], 1u);
     }
-    int incl = sum;
+    __syncthreads();
+    if (tid < 64) {
+      // lane l owns digits 255-4l .. 252-4l (descending); the lane where the running count
+      // from the top reaches `remaining` holds the threshold's digit
+      int c[4], sum = 0;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off);
-      if (lane >= off) incl += y;
-    }
-    const int excl = incl - sum;
-    int digit = 0, above = 0;
-    int run = excl;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (run < remaining && remaining <= run + c[k]) {
-        digit = 255 - 4 * lane - k;
-        above = run;
+      for (int k = 0; k < 4; ++k) {
+        c[k] = (int)s_hist[255 - 4 * tid - k];
+        sum += c[k];
       }
-      run += c[k];
+      int incl = sum;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (tid >= off) incl += y;
+      }
+      const int excl = incl - sum;
+      if (excl < remaining && remaining <= incl) {
+        int run = excl;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (run < remaining && remaining <= run + c[k]) {
+            s_digit = 255 - 4 * tid - k;
+            s_above = run;
+          }
+          run += c[k];
+        }
+      }
     }
-    const unsigned long long hit = __ballot(excl < remaining && remaining <= incl);
-    const int src = __ffsll((long long)hit) - 1;
-    digit = __shfl(digit, src);
-    above = __shfl(above, src);
-    prefix |= (uint32_t)digit << shift;
-    remaining -= above;
+    __syncthreads();
+    prefix |= (uint32_t)s_digit << shift;
+    remaining -= s_above;
+    low = shift;
   }
   const uint32_t T = prefix;   // the need-th largest key; `remaining` keys equal to T are taken
 
-  int carry_eq = 0, carry_sel = 0;
-  for (int base = 0; base < n_c; base += kSelectThreads) {
-    const int i = base + lane;
-    const uint32_t k = (i < n_c) ? key_at(i) : 0u;
-    const bool gt = (i < n_c) && k > T;
-    const bool eq = (i < n_c) && k == T;
-    const unsigned long long eqm = __ballot(eq);
-    const bool take = gt || (eq && carry_eq + __popcll(eqm & lt_mask) < remaining);
-    const unsigned long long tm = __ballot(take);
-    const int pos = carry_sel + __popcll(tm & lt_mask);
-    if (take && pos < need) idx_out[pos] = i;
-    carry_eq += __popcll(eqm);
-    carry_sel += __popcll(tm);
+  int n_eq = 0;
+#pragma unroll
+  for (int j = 0; j < kKeysPerThread; ++j) n_eq += (j < kpt && i0 + j < n_c && key[j] == T);
+  int tot;
+  int eq_rank = block_excl_scan(n_eq, s_wave, &tot);
+  int n_take = 0;
+  uint32_t take_mask = 0u;
+#pragma unroll
+  for (int j = 0; j < kKeysPerThread; ++j) {
+    const bool valid = j < kpt && i0 + j < n_c;
+    bool take = valid && key[j] > T;
+    if (valid && key[j] == T) {
+      take = eq_rank < remaining;
+      ++eq_rank;
+    }
+    take_mask |= (take ? 1u : 0u) << j;
+    n_take += take;
   }
-  for (int j = lane; j < L; j += kSelectThreads) idx_out[need + j] = n_c + j;
-  if (lane == 0) a.sel_cnt[b] = K;
+  int pos = block_excl_scan(n_take, s_wave, &tot);
+#pragma unroll
+  for (int j = 0; j < kKeysPerThread; ++j) {
+    if ((take_mask >> j) & 1u) {
+      if (pos < need) idx_out[pos] = i0 + j;
+      ++pos;
+    }
+  }
+  for (int j = tid; j < L; j += kSelectThreads) idx_out[need + j] = n_c + j;
+  if (tid == 0) a.sel_cnt[b] = K;
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {

@@ -96,6 +96,18 @@ def test_select_validation(D, sel, status):
         D.delta_workspace_bytes(shape(D), D.make_select(2048, 128, agg=2))
 
 
+def test_selection_key_limit(D):
+    # token-level units: at most 8192 candidate units per sequence
+    ok = shape(D, max_pages_per_seq=1024, max_seq_len=8192 + 128)
+    assert D.delta_workspace_bytes(ok, D.make_select(2048, 128, unit_tokens=1)) > 0
+    big = shape(D, max_pages_per_seq=1024, max_seq_len=8192 + 129)
+    with pytest.raises(D.DeltaError) as e:
+        D.delta_workspace_bytes(big, D.make_select(2048, 128, unit_tokens=1))
+    assert e.value.status == -2
+    pages = shape(D, max_pages_per_seq=8192, max_seq_len=131072)
+    assert D.delta_workspace_bytes(pages, D.make_select(2048, 128)) > 0
+
+
 def test_calls_reject_before_launch(D):
     """Every error path returns before anything reaches the (absent) GPU."""
     s = shape(D)
