@@ -10,8 +10,8 @@
 // Work decomposition.  One workgroup (4 waves) per (split, kv head g, sequence b).  A split
 // is a run of `gps` groups of 16 rows; a group is one 16-token page tile [16, D] of K and of
 // V (4 KB each at D = 128, contiguous in HBM), or 16 gathered token rows in token-level
-// sparse mode.  Waves take groups round-robin and keep their own online-softmax state, so
-// all G query heads of the KV group share every K/V byte read from HBM.
+// sparse mode.  Waves take the split's groups in interleaved blocks of four and keep their
+// own online-softmax state; all G query heads of the KV group share every K/V byte read.
 //
 // Per group and wave:
 //   * QK^T on the matrix cores: v_mfma_f32_16x16x32_bf16 with A = the 16 K rows (M = rows,
@@ -22,7 +22,9 @@
 //   * P.V on the vector ALUs: each lane owns 8 consecutive head-dim columns of 16/RPI rows
 //     (128-bit loads, one V row per LPR consecutive lanes, fully coalesced).
 //   K/V of the next group are loaded before the current one is consumed (register double
-//   buffer) so every wave keeps 8 KB of loads in flight.
+//   buffer) so every wave keeps 8 KB of loads in flight; waves interleave in blocks of four
+//   groups.  In Delta mode the logits of 256-group chunks are staged in LDS and written by the
+//   whole workgroup between chunks.
 //
 // Split combine.  The 4 waves merge through LDS into one (max, sum, o) partial per split,
 // written to the workspace.  The last workgroup of each (b, g) to arrive (device-scope fence +
@@ -201,7 +203,14 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
 
   const int Hq_row = b * Hq + g * G;
-  auto process = [&](const Tile<D>& t, int li) {
+  // Delta mode: the workgroup keeps the logits of a chunk of kChunk groups in LDS
+  // ([group][head][16], the global layout) and writes the chunk out cooperatively between
+  // chunks.  Stores complete in order with the loads issued after them, so stores inside the
+  // group loop would hold up the next prefetch; here no store precedes a prefetch in a chunk.
+  constexpr int kChunk = 256;                              // a multiple of 16
+  __shared__ float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
+  const bool want_logits = MODE == ROWS_DENSE && a.logits != nullptr;
+  auto process = [&](const Tile<D>& t, int li, int slot) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < Gm::NK; ++ks)
@@ -211,12 +220,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
-    if (MODE == ROWS_DENSE && a.logits != nullptr && hcol < G) {
-      // group-major [b][g][page][G][16]: a workgroup's logits form one contiguous stream
-      // (pages g0 .. g0+gps of its KV group), written G*64 bytes per group
-      float* lg = a.logits + ((((size_t)b * a.n_kv_heads + g) * a.logit_pages + (g0 + li)) * G + hcol) * 16 + 4 * quad;
-      *reinterpret_cast<f32x4*>(lg) = f32x4{x[0], x[1], x[2], x[3]};
-    }
+    if (want_logits && hcol < G)
+      *reinterpret_cast<f32x4*>(s_stage + (slot * G + hcol) * 16 + 4 * quad) = f32x4{x[0], x[1], x[2], x[3]};
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -271,28 +276,39 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     }
   };
 
-  // Each wave walks groups wave, wave+4, ... through a ring of three register tiles, so two
-  // groups' loads are in flight while one is consumed.  Loads past the wave's last group are
-  // clamped to that group (already requested by this wave: served by the caches).
-  if (wave < ng) {
-    const int last = wave + ((ng - 1 - wave) / kWaves) * kWaves;
-    Tile<D> t0, t1, t2;
-    int li = wave;
-    load_tile(t0, li);
-    load_tile(t1, min(li + kWaves, last));
-    while (true) {
-      load_tile(t2, min(li + 2 * kWaves, last));
-      process(t0, li);
-      li += kWaves;
-      if (li >= ng) break;
-      load_tile(t0, min(li + 2 * kWaves, last));
-      process(t1, li);
-      li += kWaves;
-      if (li >= ng) break;
-      load_tile(t1, min(li + 2 * kWaves, last));
-      process(t2, li);
-      li += kWaves;
-      if (li >= ng) break;
+  // Waves interleave in blocks of four groups (wave w takes groups 16j + 4w .. 16j + 4w + 3),
+  // so the workgroup streams about sixteen adjacent pages at a time.  Register double buffer:
+  // the next group's K/V loads are in flight while the current group is consumed; the
+  // prefetch past the wave's last group is clamped to that group (already requested: served
+  // by the caches).  The chunk loop is uniform over the workgroup (its barriers are reached by
+  // every wave); without logits there is a single chunk.
+  {
+    auto group_of = [&](int k) { return 16 * (k >> 2) + 4 * wave + (k & 3); };
+    const int full_blocks = ng / 16, rem = ng - 16 * full_blocks;
+    const int n_mine = 4 * full_blocks + min(4, max(0, rem - 4 * wave));
+    const int last = n_mine > 0 ? group_of(n_mine - 1) : 0;
+    const int chunk = want_logits ? kChunk : ng;
+    Tile<D> cur, nxt;
+    if (n_mine > 0) load_tile(cur, group_of(0));
+    int k = 0;
+    for (int c0 = 0; c0 < ng; c0 += chunk) {
+      // this wave's groups below c0 + chunk (all remaining ones in the last chunk)
+      const int kend = c0 + chunk >= ng ? n_mine : min(n_mine, ((c0 + chunk) / 16) * 4);
+      for (; k < kend; ++k) {
+        const int li = group_of(k);
+        load_tile(nxt, k + 1 < n_mine ? group_of(k + 1) : last);
+        process(cur, li, li - c0);
+        cur = nxt;
+      }
+      if (want_logits) {
+        // chunk [c0, c0 + n) goes to [b][kv group][page g0 + c0 ...][head][16], contiguous
+        __syncthreads();
+        const int n = min(chunk, ng - c0) * G * 16;
+        float* dst = a.logits + (((size_t)b * a.n_kv_heads + g) * a.logit_pages + g0 + c0) * G * 16;
+        for (int i = 4 * tid; i < n; i += 4 * kAttnThreads)
+          *reinterpret_cast<f32x4*>(dst + i) = *reinterpret_cast<const f32x4*>(s_stage + i);
+        __syncthreads();
+      }
     }
   }
 
