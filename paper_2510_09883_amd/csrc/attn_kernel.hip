@@ -23,8 +23,8 @@
 //     (128-bit loads, one V row per LPR consecutive lanes, fully coalesced).
 //   K/V of the next group are loaded before the current one is consumed (register double
 //   buffer) so every wave keeps 8 KB of loads in flight; waves interleave in blocks of four
-//   groups.  In Delta mode the logits of 256-group chunks are staged in LDS and written by the
-//   whole workgroup between chunks.
+//   groups.  In Delta mode the logits of up to 2048/G groups are staged in LDS and written by
+//   the whole workgroup between chunks.
 //
 // Split combine.  The 4 waves merge through LDS into one (max, sum, o) partial per split,
 // written to the workspace.  The last workgroup of each (b, g) to arrive (device-scope fence +
@@ -204,10 +204,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 
   const int Hq_row = b * Hq + g * G;
   // Delta mode: the workgroup keeps the logits of a chunk of kChunk groups in LDS
-  // ([group][head][16], the global layout) and writes the chunk out cooperatively between
-  // chunks.  Stores complete in order with the loads issued after them, so stores inside the
-  // group loop would hold up the next prefetch; here no store precedes a prefetch in a chunk.
-  constexpr int kChunk = 256;                              // a multiple of 16
+  // ([group][head][16], the global layout; about 128 KB) and writes the chunk out
+  // cooperatively between chunks.  Measured on MI355X, logit stores interleaved with the K/V
+  // read stream cost several times their bytes, while the same bytes written in a few large
+  // bursts (reads paused) cost about their share; so chunks are as large as LDS allows.
+  constexpr int kChunk = (2048 / G) / 16 * 16;             // a multiple of 16
   __shared__ float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
   const bool want_logits = MODE == ROWS_DENSE && a.logits != nullptr;
   auto process = [&](const Tile<D>& t, int li, int slot) {

@@ -26,7 +26,6 @@ constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kScoreThreads = 256;
 constexpr int kSelectThreads = 256;
 constexpr int kSelectWaves = kSelectThreads / 64;
-constexpr int kKeysPerThread = kMaxSelectKeys / kSelectThreads;
 
 template <int AGG, int U>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a) {
@@ -42,17 +41,17 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
     const int G = Hq / a.n_kv_heads;
     const size_t gstride = (size_t)a.logit_pages * G * 16;
     const float* row = a.logits + (size_t)b * a.n_kv_heads * gstride + (size_t)(t >> 4) * G * 16 + (t & 15);
-    // one flat loop over all heads (j = g*G + h) so that eight loads are in flight at a time
+    // one flat loop over all heads (j = g*G + h) so that sixteen loads are in flight at a time
     if (AGG == 0) {
       float m = kNegInf;
-#pragma unroll 8
+#pragma unroll 16
       for (int j = 0; j < Hq; ++j) {
         const int g = j / G, h = j - g * G;
         m = fmaxf(m, row[g * gstride + h * 16] - lse[j]);
       }
       sc = exp2f(m);
     } else {
-#pragma unroll 8
+#pragma unroll 16
       for (int j = 0; j < Hq; ++j) {
         const int g = j / G, h = j - g * G;
         sc += exp2f(row[g * gstride + h * 16] - lse[j]);
@@ -98,9 +97,10 @@ __device__ __forceinline__ int block_excl_scan(int v, int* s_wave, int* total) {
   return base + incl - v;
 }
 
-// One workgroup per sequence.  Thread t owns the candidate keys [t*kpt, t*kpt + kpt) in
-// registers (kpt <= kKeysPerThread), so index order is thread order then slot order and one
-// block scan places every chosen unit.
+// One workgroup per sequence.  Thread t owns the candidate keys [t*KPT, t*KPT + KPT) in
+// registers, so index order is thread order then slot order and one block scan places every
+// chosen unit.  KPT (keys per thread) is chosen on the host from the candidate bound.
+template <int KPT>
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -117,30 +117,31 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
     if (tid == 0) a.sel_cnt[b] = max(n_u, 0);
     return;
   }
-  const int n_c = min(n_u - L, kMaxSelectKeys);   // candidate (older) units; the host bounds it
+  const int n_c = min(n_u - L, KPT * kSelectThreads);   // candidate (older) units; the host bounds it
   const int need = K - L;       // >= 1
   const float* S = a.unit_scores + (size_t)b * a.nu_stride;
-  const int kpt = (n_c + kSelectThreads - 1) / kSelectThreads;
-  const int i0 = tid * kpt;
+  const int i0 = tid * KPT;
 
   __shared__ uint32_t s_hist[256];
   __shared__ int s_wave[kSelectWaves];
   __shared__ uint32_t s_red[2][kSelectWaves];
   __shared__ int s_digit, s_above;
 
-  uint32_t key[kKeysPerThread];
+  // unconditional loads (indices clamped into the row) so that all of them are in flight at
+  // once; slots past this thread's keys are zeroed afterwards
+  uint32_t key[KPT];
 #pragma unroll
-  for (int j = 0; j < kKeysPerThread; ++j) {
-    const int i = i0 + j;
-    key[j] = (j < kpt && i < n_c) ? key_of(S[i]) : 0u;
-  }
+  for (int j = 0; j < KPT; ++j) key[j] = key_of(S[min(i0 + j, n_c - 1)]);
+#pragma unroll
+  for (int j = 0; j < KPT; ++j)
+    if (!(i0 + j < n_c)) key[j] = 0u;
   // Bits shared by every candidate key need no histogram: start the digit passes at the
   // highest bit where two keys differ (page scores mostly share sign and high exponent bits,
   // which would otherwise send every key of the first pass to the same bin).
   uint32_t k_or = 0u, k_and = 0xffffffffu;
 #pragma unroll
-  for (int j = 0; j < kKeysPerThread; ++j) {
-    if (j < kpt && i0 + j < n_c) {
+  for (int j = 0; j < KPT; ++j) {
+    if (i0 + j < n_c) {
       k_or |= key[j];
       k_and &= key[j];
     }
@@ -173,9 +174,9 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
     s_hist[tid] = 0u;                                 // kSelectThreads == 256 bins
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kKeysPerThread; ++j) {
+    for (int j = 0; j < KPT; ++j) {
       const uint32_t k = key[j];
-      const bool match = j < kpt && i0 + j < n_c && (top >= 32 || (k >> top) == (prefix >> top));
+      const bool match = i0 + j < n_c && (top >= 32 || (k >> top) == (prefix >> top));
       if (match) atomicAdd(&s_hist[(k >> shift) & ((1u << width) - 1u)], 1u);
     }
     __syncthreads();
@@ -216,14 +217,14 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
 
   int n_eq = 0;
 #pragma unroll
-  for (int j = 0; j < kKeysPerThread; ++j) n_eq += (j < kpt && i0 + j < n_c && key[j] == T);
+  for (int j = 0; j < KPT; ++j) n_eq += (i0 + j < n_c && key[j] == T);
   int tot;
   int eq_rank = block_excl_scan(n_eq, s_wave, &tot);
   int n_take = 0;
   uint32_t take_mask = 0u;
 #pragma unroll
-  for (int j = 0; j < kKeysPerThread; ++j) {
-    const bool valid = j < kpt && i0 + j < n_c;
+  for (int j = 0; j < KPT; ++j) {
+    const bool valid = i0 + j < n_c;
     bool take = valid && key[j] > T;
     if (valid && key[j] == T) {
       take = eq_rank < remaining;
@@ -234,7 +235,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
   }
   int pos = block_excl_scan(n_take, s_wave, &tot);
 #pragma unroll
-  for (int j = 0; j < kKeysPerThread; ++j) {
+  for (int j = 0; j < KPT; ++j) {
     if ((take_mask >> j) & 1u) {
       if (pos < need) idx_out[pos] = i0 + j;
       ++pos;
@@ -265,7 +266,16 @@ hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,
 }
 
 hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(batch), dim3(kSelectThreads), 0, stream, a);
+  // keys per thread: the smallest power of two covering the candidate bound
+  const int bound = a.nu_stride - a.recent_units;
+  const dim3 grid(batch), block(kSelectThreads);
+  if (bound <= 1 * kSelectThreads) hipLaunchKernelGGL(select_kernel<1>, grid, block, 0, stream, a);
+  else if (bound <= 2 * kSelectThreads) hipLaunchKernelGGL(select_kernel<2>, grid, block, 0, stream, a);
+  else if (bound <= 4 * kSelectThreads) hipLaunchKernelGGL(select_kernel<4>, grid, block, 0, stream, a);
+  else if (bound <= 8 * kSelectThreads) hipLaunchKernelGGL(select_kernel<8>, grid, block, 0, stream, a);
+  else if (bound <= 16 * kSelectThreads) hipLaunchKernelGGL(select_kernel<16>, grid, block, 0, stream, a);
+  else if (bound <= 32 * kSelectThreads) hipLaunchKernelGGL(select_kernel<32>, grid, block, 0, stream, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
