@@ -205,9 +205,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   const int Hq_row = b * Hq + g * G;
   // Delta mode: the workgroup keeps the logits of a chunk of kChunk groups in LDS
   // ([group][head][16], the global layout; about 128 KB) and writes the chunk out
-  // cooperatively between chunks.  Measured on MI355X, logit stores interleaved with the K/V
-  // read stream cost several times their bytes, while the same bytes written in a few large
-  // bursts (reads paused) cost about their share; so chunks are as large as LDS allows.
+  // cooperatively between chunks, with non-temporal (streaming) stores.  Measured on MI355X,
+  // logit stores interleaved with the K/V read stream cost several times their bytes, while
+  // the same bytes written in a few large streaming bursts (reads paused) cost about their
+  // share; so chunks are as large as LDS allows.
   constexpr int kChunk = (2048 / G) / 16 * 16;             // a multiple of 16
   __shared__ float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
   const bool want_logits = MODE == ROWS_DENSE && a.logits != nullptr;
@@ -307,7 +308,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
         const int n = min(chunk, ng - c0) * G * 16;
         float* dst = a.logits + (((size_t)b * a.n_kv_heads + g) * a.logit_pages + g0 + c0) * G * 16;
         for (int i = 4 * tid; i < n; i += 4 * kAttnThreads)
-          *reinterpret_cast<f32x4*>(dst + i) = *reinterpret_cast<const f32x4*>(s_stage + i);
+          __builtin_nontemporal_store(*reinterpret_cast<const f32x4*>(s_stage + i),
+                                      reinterpret_cast<f32x4*>(dst + i));
         __syncthreads();
       }
     }

@@ -1,12 +1,12 @@
 // Page scoring and page selection for Delta layers (Sec. 4 "Selection mechanism" and
 // "Page-based DELTA"; App. A, Alg. 2 RefreshPages), gfx950.
 //
-// score_kernel: one thread per token.  With the Delta-layer attention's log2-domain logits
+// score_kernel: one thread per four tokens.  With the Delta-layer attention's log2-domain logits
 //   x_j(t) and per-head log-sum-exp lse_j, the softmax weight is alpha_j(t) = 2^(x_j(t) - lse_j).
 //   Token score s_t = max_j alpha_j(t) = 2^(max_j (x_j(t) - lse_j)) (exp2 is increasing, so one
 //   exp2 per token suffices), or sum_j alpha_j(t) with the sum aggregation.  Unit score
-//   S_u = sum of s_t over the unit's tokens: a 16-lane butterfly for pages, the token itself
-//   for token-level units.
+//   S_u = sum of s_t over the unit's tokens: four tokens per thread and a 4-lane butterfly for
+//   pages, the token itself for token-level units.
 //
 // select_kernel: one 256-thread workgroup per sequence, candidate keys in registers.  Units
 //   [n_u - L, n_u) are kept; among
@@ -27,46 +27,52 @@ constexpr int kScoreThreads = 256;
 constexpr int kSelectThreads = 256;
 constexpr int kSelectWaves = kSelectThreads / 64;
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One thread per four consecutive tokens (one 16-byte load per head; a page is four threads).
 template <int AGG, int U>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a) {
   const int b = blockIdx.y;
-  const int t = blockIdx.x * kScoreThreads + threadIdx.x;
+  const int t0 = (blockIdx.x * kScoreThreads + threadIdx.x) * 4;
   const int s_b = min(a.seq_lens[b], a.max_seq_len);
-  if ((int)(blockIdx.x * kScoreThreads) >= s_b) return;
+  if ((int)(blockIdx.x * kScoreThreads * 4) >= s_b) return;
   const int Hq = a.n_q_heads;
   const float* lse = a.lse + (size_t)b * Hq;
-  float sc = 0.f;
-  if (t < s_b) {
-    // group-major logits [b][g][page][h][16]: token t is row t%16 of page t/16; head j = g*G + h
+  float sc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (t0 < s_b) {
+    // group-major logits [b][g][page][h][16]: tokens t0..t0+3 are rows t0%16.. of page t0/16;
+    // head j = g*G + h
     const int G = Hq / a.n_kv_heads;
     const size_t gstride = (size_t)a.logit_pages * G * 16;
-    const float* row = a.logits + (size_t)b * a.n_kv_heads * gstride + (size_t)(t >> 4) * G * 16 + (t & 15);
-    // one flat loop over all heads (j = g*G + h) so that sixteen loads are in flight at a time
-    if (AGG == 0) {
-      float m = kNegInf;
+    const float* row = a.logits + (size_t)b * a.n_kv_heads * gstride + (size_t)(t0 >> 4) * G * 16 + (t0 & 15);
+    f32x4 acc;
+    if (AGG == 0) acc = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
+    else acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 16
-      for (int j = 0; j < Hq; ++j) {
-        const int g = j / G, h = j - g * G;
-        m = fmaxf(m, row[g * gstride + h * 16] - lse[j]);
-      }
-      sc = exp2f(m);
-    } else {
-#pragma unroll 16
-      for (int j = 0; j < Hq; ++j) {
-        const int g = j / G, h = j - g * G;
-        sc += exp2f(row[g * gstride + h * 16] - lse[j]);
+    for (int j = 0; j < Hq; ++j) {
+      const int g = j / G, h = j - g * G;
+      const f32x4 x = *reinterpret_cast<const f32x4*>(row + g * gstride + h * 16);
+      const float l = lse[j];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if (AGG == 0) acc[c] = fmaxf(acc[c], x[c] - l);
+        else acc[c] += exp2f(x[c] - l);
       }
     }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      sc[c] = (t0 + c < s_b) ? (AGG == 0 ? exp2f(acc[c]) : acc[c]) : 0.f;
   }
   float* out = a.unit_scores + (size_t)b * a.nu_stride;
   if (U == 16) {
-    sc += __shfl_xor(sc, 1);
-    sc += __shfl_xor(sc, 2);
-    sc += __shfl_xor(sc, 4);
-    sc += __shfl_xor(sc, 8);
-    if ((t & 15) == 0 && t < s_b) out[t >> 4] = sc;
+    float p = (sc[0] + sc[1]) + (sc[2] + sc[3]);
+    p += __shfl_xor(p, 1);
+    p += __shfl_xor(p, 2);
+    if ((t0 & 15) == 0 && t0 < s_b) out[t0 >> 4] = p;
   } else {
-    if (t < s_b) out[t] = sc;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (t0 + c < s_b) out[t0 + c] = sc[c];
   }
 }
 
@@ -255,7 +261,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {
 
 hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,
                         hipStream_t stream) {
-  const dim3 grid((a.max_seq_len + kScoreThreads - 1) / kScoreThreads, batch);
+  const dim3 grid((a.max_seq_len + 4 * kScoreThreads - 1) / (4 * kScoreThreads), batch);
   const dim3 block(kScoreThreads);
   if (agg == 0 && unit_tokens == 16) hipLaunchKernelGGL((score_kernel<0, 16>), grid, block, 0, stream, a);
   else if (agg == 0 && unit_tokens == 1) hipLaunchKernelGGL((score_kernel<0, 1>), grid, block, 0, stream, a);
