@@ -10,8 +10,9 @@ Infinity Cache cannot serve a step from the previous one.
 
 Printed JSON line (rank 0, N = 1): value = DELTA-stack microseconds per step (lower is
 better), with the full stack, tokens/s, algorithmic HBM GB/s, per-role layer times, the
-Delta-select overhead, the roofline of the dominant kernel (per-launch HIP-event timing on
-the launch stream) and the CPU oracle timed on this host.
+Delta-select overhead, the roofline of the dominant kernel (per-launch time from HIP events
+around graph-captured launches of that role on the launch stream) and the CPU oracle timed on
+this host.
 """
 from __future__ import annotations
 
@@ -130,62 +131,71 @@ def time_steps(stack, steps, warmup):
 
 
 def time_layers(D, w, sets, stack, shape, sel, ws, steps):
-    """Per-launch durations of each layer's entry point, HIP events on the launch stream.
-    A spin kernel ahead of the launches keeps the GPU busy while the host enqueues them, so
-    the events bracket back-to-back GPU work rather than host launch latency."""
+    """Average duration of one launch of each layer role's entry point.  For each role, the
+    role's layers of one step are captured in a HIP graph (one graph per rotating input set)
+    and replayed `steps` times between two HIP events on the launch stream; the per-launch
+    time is the elapsed time over the number of calls, so host launch latency and per-call
+    event overhead are excluded (the inter-kernel gap inside a graph is included)."""
     roles = stack.roles
     slots, cur = [], -1
     for r in roles:
         if r == configs.ROLE_DELTA:
             cur += 1
         slots.append(cur)
-    n_calls = steps * len(roles)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(n_calls)]
 
-    def call(k, i):
-        inp = sets[k % len(sets)]
-        out = stack.outs[k % len(sets)][i]
+    def role_name(i):
+        r = roles[i]
+        return "full" if (r == configs.ROLE_FULL or slots[i] < 0) else ROLE_NAME[r]
+
+    def call(si, i):
+        inp = sets[si]
+        out = stack.outs[si][i]
         kv = D.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
-        r, sd = roles[i], slots[i]
-        if r == configs.ROLE_FULL or sd < 0:
+        name, sd = role_name(i), slots[i]
+        if name == "full":
             D.delta_full_attn(shape, kv, inp.q[i], out, ws)
-        elif r == configs.ROLE_DELTA:
+        elif name == "delta":
             D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
                                       stack.sel_cnt[sd], None, ws)
         else:
             D.delta_sparse_attn(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
                                 stack.sel_cnt[sd], ws)
 
-    for i in range(len(roles)):        # warm the entry points
-        call(0, i)
-    torch.cuda.synchronize()
-    t = time.perf_counter()
+    # eager pass in layer order: every selection slot holds this step's selection
     for i in range(len(roles)):
         call(0, i)
-    enqueue_s = time.perf_counter() - t
     torch.cuda.synchronize()
-    # spin about 2x the host enqueue time of the timed calls (clock calibrated on the fly)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(); torch.cuda._sleep(1_000_000); c1.record(); torch.cuda.synchronize()
-    cyc_per_ms = 1_000_000 / max(c0.elapsed_time(c1), 1e-3)
-    torch.cuda._sleep(int(cyc_per_ms * 1e3 * enqueue_s * steps * 2 + cyc_per_ms))
-    n = 0
-    for k in range(steps):
-        for i in range(len(roles)):
-            evs[n][0].record()
-            call(k, i)
-            evs[n][1].record()
-            n += 1
-    torch.cuda.synchronize()
-    per_role = {}
-    n = 0
-    for k in range(steps):
-        for i, r in enumerate(roles):
-            name = "full" if (r == configs.ROLE_FULL or slots[i] < 0) else ROLE_NAME[r]
-            per_role.setdefault(name, []).append(evs[n][0].elapsed_time(evs[n][1]) * 1e3)
-            n += 1
-    return {k: sum(v) / len(v) for k, v in per_role.items()}, {k: len(v) // steps for k, v in per_role.items()}
+    per_role, counts = {}, {}
+    for name in ("full", "delta", "sparse"):
+        layers = [i for i in range(len(roles)) if role_name(i) == name]
+        if not layers:
+            continue
+        graphs = []
+        for si in range(len(sets)):
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                for i in layers:
+                    call(si, i)
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in layers:
+                    call(si, i)
+            graphs.append(g)
+        for r in range(2):
+            graphs[r % len(graphs)].replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for r in range(steps):
+            graphs[r % len(graphs)].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        per_role[name] = e0.elapsed_time(e1) * 1e3 / (steps * len(layers))
+        counts[name] = len(layers)
+    return per_role, counts
 
 
 # ------------------------------------------------------------------------------------------
