@@ -84,6 +84,7 @@ class Stack:
         n_delta = max(1, sum(r == configs.ROLE_DELTA for r in roles))
         self.sel_idx = torch.zeros((n_delta, w.batch, w.budget_units), dtype=torch.int32, device="cuda")
         self.sel_cnt = torch.zeros((n_delta, w.batch), dtype=torch.int32, device="cuda")
+        self.sel_phys = torch.zeros((n_delta, w.batch, w.budget_units), dtype=torch.int32, device="cuda")
         self.outs, self.args = [], []
         for inp in sets:
             outs = [torch.empty_like(q) for q in inp.q]
@@ -156,10 +157,11 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps):
             D.delta_full_attn(shape, kv, inp.q[i], out, ws)
         elif name == "delta":
             D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
-                                      stack.sel_cnt[sd], None, ws)
+                                      stack.sel_cnt[sd], None, ws, sel_phys=stack.sel_phys[sd])
         else:
+            # as in delta_decode_step: the selection's physical pages (shared page table)
             D.delta_sparse_attn(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
-                                stack.sel_cnt[sd], ws)
+                                stack.sel_cnt[sd], ws, sel_phys=stack.sel_phys[sd])
 
     # eager pass in layer order: every selection slot holds this step's selection
     for i in range(len(roles)):

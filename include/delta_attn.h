@@ -115,20 +115,29 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  *   sel_idx:     int32 [B, K] (K = budget_tokens / U): the selected logical unit indices of
  *                each sequence in ascending order; entries at and past sel_cnt[b] are -1.
  *   sel_cnt:     int32 [B]: min(K, ceil(seq_lens[b] / U)).
+ *   sel_phys:    optional int32 [B, K]: where each selected unit lives, read through
+ *                kv->page_table: its physical page (U = 16) or physical page * 16 + row
+ *                (U = 1); -1 where sel_idx is -1.  Handing it to delta_sparse_attn spares
+ *                every sparse layer that shares this page table the page-table lookup.
+ *                NULL: not written.
  *   unit_scores: optional fp32 [B, ceil(max_seq_len / U)]: S_u for u < ceil(seq_lens[b]/U);
  *                NULL keeps them in the workspace. */
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
-                            int32_t* sel_cnt, float* unit_scores, void* ws, size_t ws_bytes,
-                            void* stream);
+                            int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,
+                            size_t ws_bytes, void* stream);
 
 /* SPARSE role: attention of each query over the tokens of the selected units only, the
  * softmax renormalised over them (App. A, Alg. 1 sparse branch).  Unit u covers tokens
  * [u*U, min(u*U + U, seq_lens[b])).  sel_idx / sel_cnt as produced by
- * delta_delta_attn_select with the same `sel`.  One kernel launch. */
+ * delta_delta_attn_select with the same `sel`.  sel_phys: NULL, or the sel_phys that the
+ * same delta_delta_attn_select call wrote, valid only while kv->page_table is the page table
+ * (pointer and contents) that call read; it then replaces the page-table lookups.  One kernel
+ * launch. */
 int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                       void* out, const delta_select_t* sel, const int32_t* sel_idx,
-                      const int32_t* sel_cnt, void* ws, size_t ws_bytes, void* stream);
+                      const int32_t* sel_cnt, const int32_t* sel_phys, void* ws,
+                      size_t ws_bytes, void* stream);
 
 /* One decoding step over a layer stack (App. A, Alg. 1).  roles[i] in DELTA_ROLE_*; kv, q and
  * out are HOST arrays of n_layers entries (q[i], out[i] device pointers as above).  The
@@ -136,6 +145,8 @@ int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const vo
  * sel_idx[d] ([B, K]) and sel_cnt[d] ([B]), d counting DELTA layers from 0, and every later
  * SPARSE layer reads the most recent slot.  A SPARSE layer before the first DELTA layer
  * attends to every unit, i.e. runs FULL.  sel may be NULL only if no layer is DELTA/SPARSE.
+ * The physical locations of the current selection are kept in the workspace and used by the
+ * SPARSE layers whose kv[i].page_table pointer equals that of the DELTA layer that selected.
  * Enqueues only kernels, so the whole step can be captured into a HIP graph. */
 int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
                       const delta_kv_t* kv, const void* const* q, void* const* out,

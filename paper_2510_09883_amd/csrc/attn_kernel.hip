@@ -30,7 +30,8 @@
 // written to the workspace.  The last workgroup of each (b, g) to arrive (device-scope fence +
 // atomic counter) merges the partials in split order — a fixed order, so results do not
 // depend on arrival order — writes bf16 outputs (and the log-sum-exp), and re-arms the
-// counter to zero for the next launch.
+// counter to zero for the next launch.  A sequence that fits one split skips all of this and
+// writes its outputs directly.
 #include "internal.h"
 
 namespace delta {
@@ -115,21 +116,26 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   if (MODE == ROWS_DENSE) {
     for (int i = tid; i < cand; i += kAttnThreads) s_rows[i] = pt[g0 + i];
   } else if (MODE == ROWS_SEL_PAGE) {
+    // with precomputed physical pages the index and the page arrive together
     const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    const int32_t* phys = a.sel_phys ? a.sel_phys + (size_t)b * a.sel_stride : nullptr;
     for (int i = tid; i < cand; i += kAttnThreads) {
       const int u = sel[g0 + i];
+      const int ph = phys ? phys[g0 + i] : 0;
       const bool ok = u >= 0 && u < a.max_pages;
-      s_rows[i] = ok ? pt[u] : 0;
+      s_rows[i] = ok ? (phys ? ph : pt[u]) : 0;
       s_aux[i] = ok ? u : 0;
     }
   } else {
     const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
+    const int32_t* phys = a.sel_phys ? a.sel_phys + (size_t)b * a.sel_stride : nullptr;
     const int n_rows = min(16 * cand, a.sel_stride - 16 * g0);
     for (int i = tid; i < 16 * cand; i += kAttnThreads) {
       int packed = -1;
       if (i < n_rows) {
         const int t = sel[16 * g0 + i];
-        if (t >= 0 && t < 16 * a.max_pages) packed = pt[t >> 4] * 16 + (t & 15);
+        const int ph = phys ? phys[16 * g0 + i] : 0;
+        if (t >= 0 && t < 16 * a.max_pages) packed = phys ? ph : pt[t >> 4] * 16 + (t & 15);
       }
       s_rows[i] = packed;
     }
@@ -338,6 +344,26 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   }
   __syncthreads();
 
+  // A sequence with a single split needs no combine: the workgroup writes the output itself.
+  if (n_valid == 1) {
+    for (int idx = tid; idx < G * D; idx += kAttnThreads) {
+      const int h = idx / D, dc = idx % D;
+      float M = kNegInf;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+      float O = 0.f, L = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float f = (s_m[w][h] == kNegInf) ? 0.f : exp2f(s_m[w][h] - M);
+        O += f * s_o[w][h][dc];
+        L += f * s_l[w][h];
+      }
+      a.out[(size_t)(Hq_row + h) * D + dc] = f32_to_bf16_rne(O / L);
+      if (dc == 0 && a.lse) a.lse[(size_t)Hq_row + h] = M + log2f(L);
+    }
+    return;
+  }
+
   const size_t pbase = ((size_t)bg * a.n_split + split) * G;
   for (int idx = tid; idx < G * D; idx += kAttnThreads) {
     const int h = idx / D, dc = idx % D;
@@ -376,39 +402,65 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   __syncthreads();
   if (!s_last) return;
 
-  __shared__ float s_f[kMaxSplits][kMaxGroup];   // per split and head: exp2(m_c - M)
-  __shared__ float s_sl[kMaxSplits][kMaxGroup];  // per split and head: l_c
-  __shared__ float s_M[kMaxGroup], s_L[kMaxGroup];
+  // Each thread owns OPT outputs (head h_r, column dc_r).  The split (max, sum) pairs go to LDS
+  // while the first batch of the thread's partial outputs is already being loaded, so the
+  // combine waits for memory once when n_valid <= CB; every thread then derives its heads'
+  // running max and weights from LDS itself (no further barrier).  Splits are summed in split
+  // order: the result does not depend on the order in which workgroups finished.
+  constexpr int OPT = (G * D + kAttnThreads - 1) / kAttnThreads;
+  constexpr int CB = OPT <= 2 ? 16 : 8;
+  __shared__ float2 s_ml[kMaxSplits * kMaxGroup];
   const size_t cbase = (size_t)bg * a.n_split * G;
-  for (int i = tid; i < n_valid * G; i += kAttnThreads) {
-    const int c = i / G, h = i % G;
-    s_f[c][h] = a.part_ml[(cbase + (size_t)c * G + h) * 2 + 0];
-    s_sl[c][h] = a.part_ml[(cbase + (size_t)c * G + h) * 2 + 1];
+  for (int i = tid; i < n_valid * G; i += kAttnThreads)
+    s_ml[i] = *reinterpret_cast<const float2*>(a.part_ml + (cbase + i) * 2);
+  int h_r[OPT], dc_r[OPT];
+#pragma unroll
+  for (int r = 0; r < OPT; ++r) {
+    const int idx = min(tid + r * kAttnThreads, G * D - 1);   // clamped: duplicates not stored
+    h_r[r] = idx / D;
+    dc_r[r] = idx % D;
   }
+  float pv[OPT][CB];
+  auto load_batch = [&](int c0) {
+#pragma unroll
+    for (int r = 0; r < OPT; ++r)
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        const int cc = min(c0 + c, n_valid - 1);
+        pv[r][c] = a.part_o[(cbase + (size_t)cc * G + h_r[r]) * D + dc_r[r]];
+      }
+  };
+  load_batch(0);
   __syncthreads();
-  if (tid < G) {
-    float M = kNegInf;
-    for (int c = 0; c < n_valid; ++c) M = fmaxf(M, s_f[c][tid]);
-    s_M[tid] = M;
+  float M[OPT], L[OPT], O[OPT];
+#pragma unroll
+  for (int r = 0; r < OPT; ++r) {
+    M[r] = kNegInf;
+    for (int c = 0; c < n_valid; ++c) M[r] = fmaxf(M[r], s_ml[c * G + h_r[r]].x);
+    L[r] = 0.f;
+    O[r] = 0.f;
   }
-  __syncthreads();
-  for (int i = tid; i < n_valid * G; i += kAttnThreads) {
-    const int c = i / G, h = i % G;
-    s_f[c][h] = exp2f(s_f[c][h] - s_M[h]);
+  for (int c0 = 0; c0 < n_valid; c0 += CB) {
+    if (c0 > 0) load_batch(c0);
+#pragma unroll
+    for (int c = 0; c < CB; ++c) {
+      if (c0 + c < n_valid) {
+#pragma unroll
+        for (int r = 0; r < OPT; ++r) {
+          const float2 ml = s_ml[(c0 + c) * G + h_r[r]];
+          const float f = (ml.x == kNegInf) ? 0.f : exp2f(ml.x - M[r]);
+          L[r] += f * ml.y;
+          O[r] += f * pv[r][c];
+        }
+      }
+    }
   }
-  __syncthreads();
-  if (tid < G) {
-    float L = 0.f;
-    for (int c = 0; c < n_valid; ++c) L += s_f[c][tid] * s_sl[c][tid];
-    s_L[tid] = L;
-    if (a.lse) a.lse[(size_t)Hq_row + tid] = s_M[tid] + log2f(L);
-  }
-  __syncthreads();
-  for (int idx = tid; idx < G * D; idx += kAttnThreads) {
-    const int h = idx / D, dc = idx % D;
-    float O = 0.f;
-    for (int c = 0; c < n_valid; ++c) O += s_f[c][h] * a.part_o[(cbase + (size_t)c * G + h) * D + dc];
-    a.out[(size_t)(Hq_row + h) * D + dc] = f32_to_bf16_rne(O / s_L[h]);
+#pragma unroll
+  for (int r = 0; r < OPT; ++r) {
+    if (tid + r * kAttnThreads < G * D) {
+      a.out[(size_t)(Hq_row + h_r[r]) * D + dc_r[r]] = f32_to_bf16_rne(O[r] / L[r]);
+      if (dc_r[r] == 0 && a.lse) a.lse[(size_t)Hq_row + h_r[r]] = M[r] + log2f(L[r]);
+    }
   }
   if (tid == 0) a.counters[bg] = 0;
 }

@@ -70,7 +70,8 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
 }
 
 struct Layout {
-  size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, total = 0;
+  size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, phys = 0;
+  size_t total = 0;
   int max_split = 0;
   int logit_pages = 0;
   int nu_stride = 0;
@@ -139,6 +140,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     L->logits = off;  off = align_up(off + sizeof(float) * (size_t)s->batch * L->logit_pages * s->n_q_heads * 16);
     L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
     L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
+    L->phys = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * (sel->budget_tokens / sel->unit_tokens));
   }
   L->total = off;
   return DELTA_OK;
@@ -188,9 +190,11 @@ int run_full(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* 
                                  s->batch, st));
 }
 
+// `phys` (nullable): where the select kernel also writes the physical location of every
+// selected unit, read through this layer's page table.
 int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
               const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, float* uscores,
-              const Layout& L, char* ws, hipStream_t st) {
+              int32_t* phys, const Layout& L, char* ws, hipStream_t st) {
   AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
   a.logits = reinterpret_cast<float*>(ws + L.logits);
   a.lse = reinterpret_cast<float*>(ws + L.lse);
@@ -212,8 +216,11 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   SelectArgs xa{};
   xa.unit_scores = sa.unit_scores;
   xa.seq_lens = kv->seq_lens;
+  xa.page_table = kv->page_table;
   xa.sel_idx = sel_idx;
   xa.sel_cnt = sel_cnt;
+  xa.sel_phys = phys;
+  xa.max_pages = s->max_pages_per_seq;
   xa.nu_stride = L.nu_stride;
   xa.unit_tokens = sel->unit_tokens;
   xa.budget_units = sel->budget_tokens / sel->unit_tokens;
@@ -221,12 +228,15 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   return hip_rc(launch_select(xa, s->batch, st));
 }
 
+// `phys` (nullable): physical locations of `sel_idx` under this layer's page table, which
+// spare the kernel the page-table lookup.
 int run_sparse(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
                const delta_select_t* sel, const int32_t* sel_idx, const int32_t* sel_cnt,
-               const Layout& L, char* ws, hipStream_t st) {
+               const int32_t* phys, const Layout& L, char* ws, hipStream_t st) {
   AttnArgs a = base_args(s, kv, q, out, L, ws, L.sparse);
   a.sel_idx = sel_idx;
   a.sel_cnt = sel_cnt;
+  a.sel_phys = phys;
   a.sel_stride = sel->budget_tokens / sel->unit_tokens;
   return hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, L.sparse_mode, a,
                                  s->batch, st));
@@ -265,8 +275,8 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
 
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
-                            int32_t* sel_cnt, float* unit_scores, void* ws, size_t ws_bytes,
-                            void* stream) {
+                            int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,
+                            size_t ws_bytes, void* stream) {
   if (!sel) return DELTA_ERR_INVALID_ARG;
   Layout L;
   int rc = make_layout(shape, sel, &L);
@@ -274,13 +284,14 @@ int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, co
   if ((rc = check_kv(kv))) return rc;
   if (!q || !out || !ws || !sel_idx || !sel_cnt) return DELTA_ERR_INVALID_ARG;
   if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
-  return run_delta(shape, kv, q, out, sel, sel_idx, sel_cnt, unit_scores, L,
+  return run_delta(shape, kv, q, out, sel, sel_idx, sel_cnt, unit_scores, sel_phys, L,
                    static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
 
 int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                       void* out, const delta_select_t* sel, const int32_t* sel_idx,
-                      const int32_t* sel_cnt, void* ws, size_t ws_bytes, void* stream) {
+                      const int32_t* sel_cnt, const int32_t* sel_phys, void* ws,
+                      size_t ws_bytes, void* stream) {
   if (!sel) return DELTA_ERR_INVALID_ARG;
   Layout L;
   int rc = make_layout(shape, sel, &L);
@@ -288,8 +299,8 @@ int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const vo
   if ((rc = check_kv(kv))) return rc;
   if (!q || !out || !ws || !sel_idx || !sel_cnt) return DELTA_ERR_INVALID_ARG;
   if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
-  return run_sparse(shape, kv, q, out, sel, sel_idx, sel_cnt, L, static_cast<char*>(ws),
-                    static_cast<hipStream_t>(stream));
+  return run_sparse(shape, kv, q, out, sel, sel_idx, sel_cnt, sel_phys, L,
+                    static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
 
 int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
@@ -319,16 +330,22 @@ int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_
   const int K = sel ? sel->budget_tokens / sel->unit_tokens : 0;
   const size_t slot = (size_t)shape->batch * K;
   int cur = -1;   // most recent Delta slot; -1 = every unit (App. A, Alg. 1 initialisation)
+  // Each Delta layer also leaves the physical locations of its selection in the workspace,
+  // read through its page table; later sparse layers that share that page table use them.
+  int32_t* phys = sel ? reinterpret_cast<int32_t*>(w + L.phys) : nullptr;
+  const int32_t* phys_pt = nullptr;
   for (int i = 0; i < n_layers; ++i) {
     if (roles[i] == DELTA_ROLE_FULL || (roles[i] == DELTA_ROLE_SPARSE && cur < 0)) {
       rc = run_full(shape, &kv[i], q[i], out[i], L, w, st);
     } else if (roles[i] == DELTA_ROLE_DELTA) {
       ++cur;
       rc = run_delta(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
-                     sel_cnt + (size_t)cur * shape->batch, nullptr, L, w, st);
+                     sel_cnt + (size_t)cur * shape->batch, nullptr, phys, L, w, st);
+      phys_pt = kv[i].page_table;
     } else {
       rc = run_sparse(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
-                      sel_cnt + (size_t)cur * shape->batch, L, w, st);
+                      sel_cnt + (size_t)cur * shape->batch,
+                      kv[i].page_table == phys_pt ? phys : nullptr, L, w, st);
     }
     if (rc) return rc;
   }

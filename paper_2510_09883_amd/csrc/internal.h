@@ -27,6 +27,7 @@ struct AttnArgs {
   const int32_t* seq_lens;   // [B]
   const int32_t* sel_idx;    // [B, sel_stride] (sparse modes)
   const int32_t* sel_cnt;    // [B]             (sparse modes)
+  const int32_t* sel_phys;   // [B, sel_stride] physical locations of sel_idx, or null
   const uint16_t* q;         // bf16 [B, Hq, D]
   uint16_t* out;             // bf16 [B, Hq, D]
   float* part_o;             // [B*Hkv, n_split, G, D]   un-normalised split outputs
@@ -58,9 +59,12 @@ hipError_t launch_score(int agg, int unit_tokens, const ScoreArgs& a, int batch,
 struct SelectArgs {
   const float* unit_scores;  // [B, nu_stride]
   const int32_t* seq_lens;   // [B]
+  const int32_t* page_table; // [B, max_pages]
   int32_t* sel_idx;          // [B, budget_units]
   int32_t* sel_cnt;          // [B]
-  int32_t nu_stride, unit_tokens, budget_units, recent_units;
+  int32_t* sel_phys;         // [B, budget_units] physical page (U = 16) or page*16 + row (U = 1)
+                             // of each selected unit, -1 past the count; null: not written
+  int32_t nu_stride, unit_tokens, budget_units, recent_units, max_pages;
 };
 
 hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream);

@@ -54,9 +54,10 @@ def _bind(lib):
     lib.delta_workspace_init.argtypes = [_vp, ctypes.c_size_t, _vp]
     lib.delta_full_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.delta_delta_attn_select.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp,
-                                            _P(delta_select_t), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+                                            _P(delta_select_t), _vp, _vp, _vp, _vp, _vp,
+                                            ctypes.c_size_t, _vp]
     lib.delta_sparse_attn.argtypes = [_P(delta_shape_t), _P(delta_kv_t), _vp, _vp, _P(delta_select_t),
-                                      _vp, _vp, _vp, ctypes.c_size_t, _vp]
+                                      _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.delta_decode_step.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
                                       _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
                                       _vp, _vp, _vp, ctypes.c_size_t, _vp]
@@ -135,18 +136,20 @@ def delta_full_attn(shape, kv: delta_kv_t, q, out, ws):
                                                    _ptr(out), _ptr(ws), _nbytes(ws), _stream()))
 
 
-def delta_delta_attn_select(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, unit_scores, ws):
+def delta_delta_attn_select(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, unit_scores, ws,
+                            sel_phys=None):
     _check("delta_delta_attn_select",
            _lib.delta_delta_attn_select(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
                                         ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt),
-                                        _ptr(unit_scores), _ptr(ws), _nbytes(ws), _stream()))
+                                        _ptr(sel_phys), _ptr(unit_scores), _ptr(ws), _nbytes(ws),
+                                        _stream()))
 
 
-def delta_sparse_attn(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, ws):
+def delta_sparse_attn(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, ws, sel_phys=None):
     _check("delta_sparse_attn",
            _lib.delta_sparse_attn(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
-                                  ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt), _ptr(ws),
-                                  _nbytes(ws), _stream()))
+                                  ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt), _ptr(sel_phys),
+                                  _ptr(ws), _nbytes(ws), _stream()))
 
 
 class StepArgs:

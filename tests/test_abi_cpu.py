@@ -120,9 +120,9 @@ def test_calls_reject_before_launch(D):
     assert lib.delta_full_attn(P(s), P(kv), fake, fake, fake, 16, None) == -3
     assert lib.delta_full_attn(P(s), None, fake, fake, fake, need, None) == -1
     assert lib.delta_full_attn(P(s), P(kv), None, fake, fake, need, None) == -1
-    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, P(sel), None, fake, None, fake, need, None) == -1
-    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, None, fake, fake, None, fake, need, None) == -1
-    assert lib.delta_sparse_attn(P(s), P(kv), fake, fake, P(sel), fake, fake, fake, need - 1, None) == -3
+    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, P(sel), None, fake, None, None, fake, need, None) == -1
+    assert lib.delta_delta_attn_select(P(s), P(kv), fake, fake, None, fake, fake, None, None, fake, need, None) == -1
+    assert lib.delta_sparse_attn(P(s), P(kv), fake, fake, P(sel), fake, fake, None, fake, need - 1, None) == -3
     bad = D.make_shape(2, 32, 8, 80, 512, 8192)
     assert lib.delta_full_attn(P(bad), P(kv), fake, fake, fake, need, None) == -2
     roles = (ctypes.c_int32 * 3)(0, 1, 2)

@@ -79,6 +79,43 @@ def test_config1_standalone_entry_points_and_scores():
     assert ok, err
 
 
+@pytest.mark.parametrize("U", [16, 1])
+def test_physical_selection_matches_page_table(U):
+    """sel_phys is sel_idx read through the page table (exactly, -1 padding included), and a
+    sparse layer given sel_phys computes bit for bit what it computes through the page table.
+    Lengths mix sequences that fit the budget (every unit kept) with ones that select."""
+    d = D()
+    w = configs.get(1, U)
+    lens = [1024, 100, 129, 1000]
+    w.batch = len(lens)
+    inp = synth.make_inputs(w, "cuda", seq_lens=lens)
+    shape, sel = shape_of(inp), select_of(w)
+    ws = d.alloc_workspace(shape, sel)
+    kv = d.make_kv(inp.k_cache[1], inp.v_cache[1], inp.page_table, inp.seq_lens)
+    K = w.budget_tokens // U
+    sel_idx = torch.empty((w.batch, K), dtype=torch.int32, device="cuda")
+    sel_cnt = torch.empty((w.batch,), dtype=torch.int32, device="cuda")
+    sel_phys = torch.full((w.batch, K), -7, dtype=torch.int32, device="cuda")
+    out_d = torch.empty_like(inp.q[1])
+    d.delta_delta_attn_select(shape, kv, inp.q[1], out_d, sel, sel_idx, sel_cnt, None, ws,
+                              sel_phys=sel_phys)
+    torch.cuda.synchronize()
+    idx, ph, pt = sel_idx.cpu().numpy(), sel_phys.cpu().numpy(), inp.page_table.cpu().numpy()
+    for b in range(w.batch):
+        valid = idx[b] >= 0
+        assert valid.sum() == int(sel_cnt[b])
+        u = idx[b][valid]
+        want = pt[b][u] if U == 16 else pt[b][u // 16] * 16 + u % 16
+        np.testing.assert_array_equal(ph[b][valid], want)
+        assert np.all(ph[b][~valid] == -1)
+    kv2 = d.make_kv(inp.k_cache[2], inp.v_cache[2], inp.page_table, inp.seq_lens)
+    out_a, out_b = torch.empty_like(inp.q[2]), torch.empty_like(inp.q[2])
+    d.delta_sparse_attn(shape, kv2, inp.q[2], out_a, sel, sel_idx, sel_cnt, ws)
+    d.delta_sparse_attn(shape, kv2, inp.q[2], out_b, sel, sel_idx, sel_cnt, ws, sel_phys=sel_phys)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16))
+
+
 # ------------------------------------------------------------------------------------------
 # Config 2 (Llama-8B shape, B=1, 8k): every layer of the step
 # ------------------------------------------------------------------------------------------
