@@ -33,6 +33,7 @@
 // counter to zero for the next launch.  A sequence that fits one split skips all of this and
 // writes its outputs directly.
 #include "internal.h"
+#include "wave.h"
 
 namespace delta {
 namespace {
@@ -231,8 +232,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     if (want_logits && hcol < G)
       *reinterpret_cast<f32x4*>(s_stage + (slot * G + hcol) * 16 + 4 * quad) = f32x4{x[0], x[1], x[2], x[3]};
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_xor32(max_xor16(mx));
     const float m_new = fmaxf(m_run, mx);
     // m_new is finite whenever the group has a valid row (always, for valid selections); the
     // guard keeps an all-masked group from turning the running state into NaN
@@ -244,8 +244,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       p[r] = exp2f(x[r] - m_use);
       ps += p[r];
     }
-    ps += __shfl_xor(ps, 16);
-    ps += __shfl_xor(ps, 32);
+    ps = sum_xor32(sum_xor16(ps));
     l_run = l_run * alpha + ps;
     m_run = m_new;
 
@@ -323,11 +322,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 
   // ---- reduce o over the lanes that share a head-dim chunk -------------------------------
 #pragma unroll
-  for (int off = Gm::LPR; off < 64; off <<= 1)
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] += __shfl_xor(o[h][e], off);
+    for (int e = 0; e < 8; ++e) {
+      float v = o[h][e];
+      if (Gm::LPR == 8) v += lane_xor8(v);
+      o[h][e] = sum_xor32(sum_xor16(v));
+    }
 
   // ---- merge the 4 waves into one split partial ------------------------------------------
   __shared__ float s_m[kWaves][kMaxGroup], s_l[kWaves][kMaxGroup];
@@ -408,7 +409,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   // running max and weights from LDS itself (no further barrier).  Splits are summed in split
   // order: the result does not depend on the order in which workgroups finished.
   constexpr int OPT = (G * D + kAttnThreads - 1) / kAttnThreads;
-  constexpr int CB = OPT <= 2 ? 16 : 8;
+  constexpr int CB = OPT <= 2 ? 32 : 16;
   __shared__ float2 s_ml[kMaxSplits * kMaxGroup];
   const size_t cbase = (size_t)bg * a.n_split * G;
   for (int i = tid; i < n_valid * G; i += kAttnThreads)

@@ -35,12 +35,14 @@ int target_workgroups() {
   return v;
 }
 
-// Minimum 16-row groups per split (per workgroup of 4 waves): two per wave.
+// Minimum 16-row groups per split (per workgroup of 4 waves): four per wave.  Small launches
+// (one sequence, a few hundred pages) measured faster with fewer, longer splits: the split
+// combine costs more per extra split than the shorter loop saves.
 int min_groups_per_split() {
   static int v = [] {
     const char* e = getenv("DELTA_ATTN_MIN_GPS");
     int x = e ? atoi(e) : 0;
-    return x > 0 ? x : 8;
+    return x > 0 ? x : 16;
   }();
   return v;
 }

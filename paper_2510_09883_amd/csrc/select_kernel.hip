@@ -18,6 +18,7 @@
 //   takes every key > T and the lowest-index keys == T (one block prefix sum), writing them in
 //   ascending order.  While n_u <= K every unit is kept.
 #include "internal.h"
+#include "wave.h"
 
 namespace delta {
 namespace {
@@ -102,8 +103,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
   float* out = a.unit_scores + (size_t)b * a.nu_stride;
   if (U == 16) {
     float p = (sc[0] + sc[1]) + (sc[2] + sc[3]);
-    p += __shfl_xor(p, 1);
-    p += __shfl_xor(p, 2);
+    p += lane_xor1(p);
+    p += lane_xor2(p);
     if ((t0 & 15) == 0 && t0 < s_b) out[t0 >> 4] = p;
   } else {
 #pragma unroll
@@ -120,12 +121,7 @@ __device__ __forceinline__ uint32_t key_of(float f) {
 // be reused by another scan); *total gets the sum.
 __device__ __forceinline__ int block_excl_scan(int v, int* s_wave, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int incl = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(incl, off);
-    if (lane >= off) incl += y;
-  }
+  const int incl = wave_incl_scan(v);
   if (lane == 63) s_wave[w] = incl;
   __syncthreads();
   int base = 0, tot = 0;
@@ -159,6 +155,23 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
   const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
   auto phys_of = [&](int u) { return U == 16 ? pt[u] : pt[u >> 4] * 16 + (u & 15); };
 
+  const float* S = a.unit_scores + (size_t)b * a.nu_stride;
+  const int i0 = tid * KPT;
+  // The keys and their page-table entries are requested before the sequence length arrives
+  // (indices clamped into the rows, so every load is in bounds): one wait for memory instead of
+  // two.  Slots past the candidates are masked once the length is known.
+  uint32_t key[KPT];
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) key[j] = key_of(S[min(i0 + j, a.nu_stride - 1)]);
+  // page-table entries of the keys (U = 1: KPT consecutive tokens span at most KPT/16 + 1 pages)
+  constexpr int NP = U == 16 ? KPT : (KPT + 15) / 16 + 1;
+  int pg[NP];
+  if (phys_out) {
+#pragma unroll
+    for (int j = 0; j < NP; ++j)
+      pg[j] = pt[min((U == 16 ? i0 : i0 >> 4) + j, a.max_pages - 1)];
+  }
+
   if (n_u <= K) {   // the context fits the budget: keep every unit
     for (int i = tid; i < K; i += kSelectThreads) {
       idx_out[i] = (i < n_u) ? i : -1;
@@ -169,29 +182,13 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
   }
   const int n_c = min(n_u - L, KPT * kSelectThreads);   // candidate (older) units; the host bounds it
   const int need = K - L;       // >= 1
-  const float* S = a.unit_scores + (size_t)b * a.nu_stride;
-  const int i0 = tid * KPT;
+  const int rec_phys = (phys_out && tid < L) ? phys_of(n_c + tid) : 0;
 
   // Histograms rotate over three buffers: the one a pass fills was cleared two passes before,
   // so each digit pass needs a single barrier.
   __shared__ uint32_t s_hist[3][256];
   __shared__ int s_wave[kSelectWaves];
   __shared__ uint32_t s_red[2][kSelectWaves];
-
-  // unconditional loads (indices clamped into the row) so that all of them are in flight at
-  // once; slots past this thread's keys are zeroed afterwards
-  uint32_t key[KPT];
-#pragma unroll
-  for (int j = 0; j < KPT; ++j) key[j] = key_of(S[min(i0 + j, n_c - 1)]);
-  // page-table entries of the keys (U = 1: KPT consecutive tokens span at most KPT/16 + 1 pages)
-  constexpr int NP = U == 16 ? KPT : (KPT + 15) / 16 + 1;
-  int pg[NP];
-  if (phys_out) {
-#pragma unroll
-    for (int j = 0; j < NP; ++j)
-      pg[j] = U == 16 ? pt[min(i0 + j, n_c - 1)] : pt[min((i0 >> 4) + j, (n_c - 1) >> 4)];
-  }
-  const int rec_phys = (phys_out && tid < L) ? phys_of(n_c + tid) : 0;
 #pragma unroll
   for (int j = 0; j < KPT; ++j)
     if (!(i0 + j < n_c)) key[j] = 0u;
@@ -208,11 +205,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
       k_and &= key[j];
     }
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    k_or |= (uint32_t)__shfl_xor((int)k_or, off);
-    k_and &= (uint32_t)__shfl_xor((int)k_and, off);
-  }
+  k_or = wave_or(k_or);
+  k_and = wave_and(k_and);
   if (lane == 0) {
     s_red[0][tid >> 6] = k_or;
     s_red[1][tid >> 6] = k_and;
@@ -250,12 +244,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
       c[k] = (int)hist[255 - 4 * lane - k];
       sum += c[k];
     }
-    int incl = sum;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off);
-      if (lane >= off) incl += y;
-    }
+    const int incl = wave_incl_scan(sum);
     const int excl = incl - sum;
     int digit = 0, above = 0, run = excl;
 #pragma unroll
@@ -267,9 +256,9 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
       run += c[k];
     }
     const uint64_t owner = __ballot(excl < remaining && remaining <= incl);
-    const int src = __ffsll((unsigned long long)owner) - 1;
-    digit = __shfl(digit, src);
-    above = __shfl(above, src);
+    const int src = __ffsll((unsigned long long)owner) - 1;   // exactly one lane owns it
+    digit = __builtin_amdgcn_readlane(digit, src);
+    above = __builtin_amdgcn_readlane(above, src);
     prefix |= (uint32_t)digit << shift;
     remaining -= above;
     low = shift;
