@@ -132,11 +132,15 @@ def time_steps(stack, steps, warmup):
 
 
 def time_layers(D, w, sets, stack, shape, sel, ws, steps):
-    """Average duration of one launch of each layer role's entry point.  For each role, the
-    role's layers of one step are captured in a HIP graph (one graph per rotating input set)
-    and replayed `steps` times between two HIP events on the launch stream; the per-launch
-    time is the elapsed time over the number of calls, so host launch latency and per-call
-    event overhead are excluded (the inter-kernel gap inside a graph is included)."""
+    """Average duration of one launch of each role's entry point.  For each role, every layer
+    of the stack runs that role (its own K/V cache and query), the n launches of one step are
+    captured in a HIP graph (one graph per rotating input set), and the graphs are replayed
+    `steps` times between two HIP events on the launch stream; per-launch time = elapsed time
+    over the number of launches.  Host launch latency and per-call event overhead are excluded;
+    the gap between kernels inside a graph is included.  Sparse launches use the selection of
+    the Delta layer that precedes them in the schedule (the first Delta layer's for layers
+    before it), with its physical pages, as delta_decode_step does.  Also returns how many
+    layers of the step run each role."""
     roles = stack.roles
     slots, cur = [], -1
     for r in roles:
@@ -144,47 +148,56 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps):
             cur += 1
         slots.append(cur)
 
-    def role_name(i):
+    def step_role(i):
         r = roles[i]
         return "full" if (r == configs.ROLE_FULL or slots[i] < 0) else ROLE_NAME[r]
 
-    def call(si, i):
+    counts = {}
+    for i in range(len(roles)):
+        counts[step_role(i)] = counts.get(step_role(i), 0) + 1
+    # every selection slot holds this step's selection and its physical pages
+    for i, r in enumerate(roles):
+        if r == configs.ROLE_DELTA:
+            inp = sets[0]
+            kv = D.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
+            D.delta_delta_attn_select(shape, kv, inp.q[i], stack.outs[0][i], sel, stack.sel_idx[slots[i]],
+                                      stack.sel_cnt[slots[i]], None, ws, sel_phys=stack.sel_phys[slots[i]])
+    torch.cuda.synchronize()
+    scratch_idx = torch.empty_like(stack.sel_idx[0])
+    scratch_cnt = torch.empty_like(stack.sel_cnt[0])
+    scratch_phys = torch.empty_like(stack.sel_phys[0])
+
+    def call(name, si, i):
         inp = sets[si]
         out = stack.outs[si][i]
         kv = D.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
-        name, sd = role_name(i), slots[i]
         if name == "full":
             D.delta_full_attn(shape, kv, inp.q[i], out, ws)
         elif name == "delta":
-            D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
-                                      stack.sel_cnt[sd], None, ws, sel_phys=stack.sel_phys[sd])
+            D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel, scratch_idx, scratch_cnt, None,
+                                      ws, sel_phys=scratch_phys)
         else:
-            # as in delta_decode_step: the selection's physical pages (shared page table)
-            D.delta_sparse_attn(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd],
-                                stack.sel_cnt[sd], ws, sel_phys=stack.sel_phys[sd])
+            sd = max(slots[i], 0)
+            D.delta_sparse_attn(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd], stack.sel_cnt[sd],
+                                ws, sel_phys=stack.sel_phys[sd])
 
-    # eager pass in layer order: every selection slot holds this step's selection
-    for i in range(len(roles)):
-        call(0, i)
-    torch.cuda.synchronize()
-    per_role, counts = {}, {}
+    per_role = {}
     for name in ("full", "delta", "sparse"):
-        layers = [i for i in range(len(roles)) if role_name(i) == name]
-        if not layers:
+        if name not in counts:
             continue
         graphs = []
         for si in range(len(sets)):
             s = torch.cuda.Stream()
             s.wait_stream(torch.cuda.current_stream())
             with torch.cuda.stream(s):
-                for i in layers:
-                    call(si, i)
+                for i in range(len(roles)):
+                    call(name, si, i)
             torch.cuda.current_stream().wait_stream(s)
             torch.cuda.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                for i in layers:
-                    call(si, i)
+                for i in range(len(roles)):
+                    call(name, si, i)
             graphs.append(g)
         for r in range(2):
             graphs[r % len(graphs)].replay()
@@ -195,8 +208,7 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps):
             graphs[r % len(graphs)].replay()
         e1.record()
         torch.cuda.synchronize()
-        per_role[name] = e0.elapsed_time(e1) * 1e3 / (steps * len(layers))
-        counts[name] = len(layers)
+        per_role[name] = e0.elapsed_time(e1) * 1e3 / (steps * len(roles))
     return per_role, counts
 
 

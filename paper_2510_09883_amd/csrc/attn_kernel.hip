@@ -160,7 +160,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   }
   if (split >= n_valid) return;
   const int ng = min(a.gps, n_groups - g0);
-  __syncthreads();
+  lds_barrier();   // the page / row list is in LDS; the query loads may still be in flight
 
   const size_t head_off = (size_t)g * 16 * D;
   auto load_tile = [&](Tile<D>& t, int li) {
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   // the same bytes written in a few large streaming bursts (reads paused) cost about their
   // share; so chunks are as large as LDS allows.
   constexpr int kChunk = (2048 / G) / 16 * 16;             // a multiple of 16
-  __shared__ float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
+  __shared__ __attribute__((aligned(16))) float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
   const bool want_logits = MODE == ROWS_DENSE && a.logits != nullptr;
   auto process = [&](const Tile<D>& t, int li, int slot) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -309,13 +309,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       }
       if (want_logits) {
         // chunk [c0, c0 + n) goes to [b][kv group][page g0 + c0 ...][head][16], contiguous
-        __syncthreads();
+        lds_barrier();
         const int n = min(chunk, ng - c0) * G * 16;
         float* dst = a.logits + (((size_t)b * a.n_kv_heads + g) * a.logit_pages + g0 + c0) * G * 16;
         for (int i = 4 * tid; i < n; i += 4 * kAttnThreads)
           __builtin_nontemporal_store(*reinterpret_cast<const f32x4*>(s_stage + i),
                                       reinterpret_cast<f32x4*>(dst + i));
-        __syncthreads();
+        lds_barrier();
       }
     }
   }
@@ -332,7 +332,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 
   // ---- merge the 4 waves into one split partial ------------------------------------------
   __shared__ float s_m[kWaves][kMaxGroup], s_l[kWaves][kMaxGroup];
-  __shared__ float s_o[kWaves][G][D];
+  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][D];
+  static_assert(G * D <= 4 * kAttnThreads && D % 4 == 0, "four outputs per thread cover a group");
   if (quad == 0 && hcol < G) {
     s_m[wave][hcol] = m_run;
     s_l[wave][hcol] = l_run;
@@ -343,46 +344,46 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) s_o[wave][h][8 * lane + e] = o[h][e];
   }
-  __syncthreads();
+  lds_barrier();
+
+  // From here on thread t owns the four consecutive outputs e0 = 4t .. 4t+3 of head h (D is a
+  // multiple of 4, G * D <= 1024 = 4 * kAttnThreads), so every partial, output and merge access
+  // is one 16- or 8-byte access and each thread needs the running max and sum of one head.
+  const int e0 = 4 * tid;
+  const bool owner = e0 < G * D;
+  const int h = owner ? e0 / D : 0;
+  const int dc = owner ? e0 % D : 0;
+  float M = kNegInf, L = 0.f;
+  f32x4 O = {0.f, 0.f, 0.f, 0.f};
+  if (owner) {
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = (s_m[w][h] == kNegInf) ? 0.f : exp2f(s_m[w][h] - M);
+      const f32x4 ow = *reinterpret_cast<const f32x4*>(&s_o[w][h][dc]);
+      O += f * ow;
+      L += f * s_l[w][h];
+    }
+  }
+  auto store_out = [&](const f32x4& v, float lsum, float mx) {
+    uint2 packed;
+    packed.x = (uint32_t)f32_to_bf16_rne(v[0] / lsum) | ((uint32_t)f32_to_bf16_rne(v[1] / lsum) << 16);
+    packed.y = (uint32_t)f32_to_bf16_rne(v[2] / lsum) | ((uint32_t)f32_to_bf16_rne(v[3] / lsum) << 16);
+    *reinterpret_cast<uint2*>(a.out + (size_t)(Hq_row + h) * D + dc) = packed;
+    if (dc == 0 && a.lse) a.lse[(size_t)Hq_row + h] = mx + log2f(lsum);
+  };
 
   // A sequence with a single split needs no combine: the workgroup writes the output itself.
   if (n_valid == 1) {
-    for (int idx = tid; idx < G * D; idx += kAttnThreads) {
-      const int h = idx / D, dc = idx % D;
-      float M = kNegInf;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
-      float O = 0.f, L = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const float f = (s_m[w][h] == kNegInf) ? 0.f : exp2f(s_m[w][h] - M);
-        O += f * s_o[w][h][dc];
-        L += f * s_l[w][h];
-      }
-      a.out[(size_t)(Hq_row + h) * D + dc] = f32_to_bf16_rne(O / L);
-      if (dc == 0 && a.lse) a.lse[(size_t)Hq_row + h] = M + log2f(L);
-    }
+    if (owner) store_out(O, L, M);
     return;
   }
 
   const size_t pbase = ((size_t)bg * a.n_split + split) * G;
-  for (int idx = tid; idx < G * D; idx += kAttnThreads) {
-    const int h = idx / D, dc = idx % D;
-    float M = kNegInf;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
-    float O = 0.f, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float f = (s_m[w][h] == kNegInf) ? 0.f : exp2f(s_m[w][h] - M);
-      O += f * s_o[w][h][dc];
-      L += f * s_l[w][h];
-    }
-    a.part_o[(pbase + h) * D + dc] = O;
-    if (dc == 0) {
-      a.part_ml[(pbase + h) * 2 + 0] = M;
-      a.part_ml[(pbase + h) * 2 + 1] = L;
-    }
+  if (owner) {
+    *reinterpret_cast<f32x4*>(a.part_o + (pbase + h) * D + dc) = O;
+    if (dc == 0) *reinterpret_cast<float2*>(a.part_ml + (pbase + h) * 2) = make_float2(M, L);
   }
 
   // ---- last workgroup of (b, g) merges the splits -----------------------------------------
@@ -403,66 +404,43 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   __syncthreads();
   if (!s_last) return;
 
-  // Each thread owns OPT outputs (head h_r, column dc_r).  The split (max, sum) pairs go to LDS
-  // while the first batch of the thread's partial outputs is already being loaded, so the
-  // combine waits for memory once when n_valid <= CB; every thread then derives its heads'
-  // running max and weights from LDS itself (no further barrier).  Splits are summed in split
-  // order: the result does not depend on the order in which workgroups finished.
-  constexpr int OPT = (G * D + kAttnThreads - 1) / kAttnThreads;
-  constexpr int CB = OPT <= 2 ? 32 : 16;
-  __shared__ float2 s_ml[kMaxSplits * kMaxGroup];
+  // The split (max, sum) pairs go to LDS while the first batch of the thread's partial outputs
+  // is already being loaded (one wait for memory when n_valid <= kMergeBatch); each thread then
+  // derives its head's max and weights from LDS itself.  Splits are summed in split order: the
+  // result does not depend on the order in which workgroups finished.
+  constexpr int kMergeBatch = 16;
+  __shared__ __attribute__((aligned(16))) float2 s_ml[kMaxSplits * kMaxGroup];
   const size_t cbase = (size_t)bg * a.n_split * G;
   for (int i = tid; i < n_valid * G; i += kAttnThreads)
     s_ml[i] = *reinterpret_cast<const float2*>(a.part_ml + (cbase + i) * 2);
-  int h_r[OPT], dc_r[OPT];
-#pragma unroll
-  for (int r = 0; r < OPT; ++r) {
-    const int idx = min(tid + r * kAttnThreads, G * D - 1);   // clamped: duplicates not stored
-    h_r[r] = idx / D;
-    dc_r[r] = idx % D;
-  }
-  float pv[OPT][CB];
+  f32x4 pv[kMergeBatch];
   auto load_batch = [&](int c0) {
 #pragma unroll
-    for (int r = 0; r < OPT; ++r)
-#pragma unroll
-      for (int c = 0; c < CB; ++c) {
-        const int cc = min(c0 + c, n_valid - 1);
-        pv[r][c] = a.part_o[(cbase + (size_t)cc * G + h_r[r]) * D + dc_r[r]];
-      }
+    for (int c = 0; c < kMergeBatch; ++c) {
+      const int cc = min(c0 + c, n_valid - 1);
+      pv[c] = *reinterpret_cast<const f32x4*>(a.part_o + (cbase + (size_t)cc * G + h) * D + dc);
+    }
   };
-  load_batch(0);
-  __syncthreads();
-  float M[OPT], L[OPT], O[OPT];
-#pragma unroll
-  for (int r = 0; r < OPT; ++r) {
-    M[r] = kNegInf;
-    for (int c = 0; c < n_valid; ++c) M[r] = fmaxf(M[r], s_ml[c * G + h_r[r]].x);
-    L[r] = 0.f;
-    O[r] = 0.f;
-  }
-  for (int c0 = 0; c0 < n_valid; c0 += CB) {
+  if (owner) load_batch(0);
+  lds_barrier();   // s_ml is in LDS; the partial outputs may still be arriving
+  if (!owner) return;
+  M = kNegInf;
+  for (int c = 0; c < n_valid; ++c) M = fmaxf(M, s_ml[c * G + h].x);
+  L = 0.f;
+  O = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < n_valid; c0 += kMergeBatch) {
     if (c0 > 0) load_batch(c0);
 #pragma unroll
-    for (int c = 0; c < CB; ++c) {
+    for (int c = 0; c < kMergeBatch; ++c) {
       if (c0 + c < n_valid) {
-#pragma unroll
-        for (int r = 0; r < OPT; ++r) {
-          const float2 ml = s_ml[(c0 + c) * G + h_r[r]];
-          const float f = (ml.x == kNegInf) ? 0.f : exp2f(ml.x - M[r]);
-          L[r] += f * ml.y;
-          O[r] += f * pv[r][c];
-        }
+        const float2 ml = s_ml[(c0 + c) * G + h];
+        const float f = (ml.x == kNegInf) ? 0.f : exp2f(ml.x - M);
+        L += f * ml.y;
+        O += f * pv[c];
       }
     }
   }
-#pragma unroll
-  for (int r = 0; r < OPT; ++r) {
-    if (tid + r * kAttnThreads < G * D) {
-      a.out[(size_t)(Hq_row + h_r[r]) * D + dc_r[r]] = f32_to_bf16_rne(O[r] / L[r]);
-      if (dc_r[r] == 0 && a.lse) a.lse[(size_t)Hq_row + h_r[r]] = M[r] + log2f(L[r]);
-    }
-  }
+  store_out(O, L, M);
   if (tid == 0) a.counters[bg] = 0;
 }
 

@@ -47,6 +47,19 @@ int min_groups_per_split() {
   return v;
 }
 
+// Most splits per (sequence, kv head).  The last workgroup's merge reads every split's partial
+// and each split adds a device-scope release and an arrival to the same counter, so beyond ~16
+// splits the combine costs more than the shorter loop saves (measured on MI355X with one
+// sequence of 8K tokens).  DELTA_ATTN_MAX_SPLITS overrides it for tuning.
+int max_splits() {
+  static int v = [] {
+    const char* e = getenv("DELTA_ATTN_MAX_SPLITS");
+    int x = e ? atoi(e) : 0;
+    return x > 0 ? std::min(x, kMaxSplits) : 16;
+  }();
+  return v;
+}
+
 struct SplitPlan {
   int n_split = 0;
   int gps = 0;
@@ -60,7 +73,7 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
   if (max_groups < 1) max_groups = 1;
   int want = std::max(1, ceil_div(target_workgroups(), pairs));
   int most = std::max(1, ceil_div(max_groups, min_groups_per_split()));
-  int n_split = std::min(std::min(want, most), kMaxSplits);
+  int n_split = std::min(std::min(want, most), max_splits());
   int gps = ceil_div(max_groups, n_split);
   if (gps > slot_cap) gps = slot_cap;
   n_split = ceil_div(max_groups, gps);

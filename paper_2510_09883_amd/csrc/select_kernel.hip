@@ -13,8 +13,10 @@
 //   [n_u - L, n_u) are kept; among
 //   the n_u - L older units the (K - L) largest scores are found by an exact radix select on
 //   the float bit patterns (non-negative floats order like their uint32 bits): after skipping
-//   the leading bits common to all keys, 8-bit digit histograms in LDS give the exact
-//   threshold key T and how many keys equal to T are needed.  A final pass in index order
+//   the leading bits common to all keys, 8-bit digit histograms in LDS narrow the threshold
+//   key T down until either every bit is fixed or all keys in the threshold's bin are needed
+//   (then the remaining bits cannot change the set), and give how many keys equal to T are
+//   needed.  A final pass in index order
 //   takes every key > T and the lowest-index keys == T (one block prefix sum), writing them in
 //   ascending order.  While n_u <= K every unit is kept.
 #include "internal.h"
@@ -88,7 +90,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
     }
   }
   s_part[wave][lane] = acc;
-  __syncthreads();
+  lds_barrier();
   if (wave != 0) return;
 #pragma unroll
   for (int w = 1; w < kScoreWaves; ++w) {
@@ -123,7 +125,7 @@ __device__ __forceinline__ int block_excl_scan(int v, int* s_wave, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int incl = wave_incl_scan(v);
   if (lane == 63) s_wave[w] = incl;
-  __syncthreads();
+  lds_barrier();
   int base = 0, tot = 0;
 #pragma unroll
   for (int i = 0; i < kSelectWaves; ++i) {
@@ -211,7 +213,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
     s_red[0][tid >> 6] = k_or;
     s_red[1][tid >> 6] = k_and;
   }
-  __syncthreads();
+  lds_barrier();
   k_or = 0u;
   k_and = 0xffffffffu;
 #pragma unroll
@@ -234,7 +236,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
       const bool match = i0 + j < n_c && (top >= 32 || (k >> top) == (prefix >> top));
       if (match) atomicAdd(&hist[(k >> shift) & ((1u << width) - 1u)], 1u);
     }
-    __syncthreads();
+    lds_barrier();
     s_hist[(pass + 2) % 3][tid] = 0u;   // for pass + 2 (last read before this pass's barrier)
     // Every wave finds the digit itself: lane l owns digits 255-4l .. 252-4l (descending); the
     // lane where the running count from the top reaches `remaining` holds the threshold digit.
@@ -246,12 +248,13 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
     }
     const int incl = wave_incl_scan(sum);
     const int excl = incl - sum;
-    int digit = 0, above = 0, run = excl;
+    int digit = 0, above = 0, count = 0, run = excl;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (run < remaining && remaining <= run + c[k]) {
         digit = 255 - 4 * lane - k;
         above = run;
+        count = c[k];
       }
       run += c[k];
     }
@@ -259,11 +262,17 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
     const int src = __ffsll((unsigned long long)owner) - 1;   // exactly one lane owns it
     digit = __builtin_amdgcn_readlane(digit, src);
     above = __builtin_amdgcn_readlane(above, src);
+    count = __builtin_amdgcn_readlane(count, src);
     prefix |= (uint32_t)digit << shift;
     remaining -= above;
     low = shift;
+    // Every key of the threshold's bin is needed: the bits below `low` cannot change the set.
+    if (count == remaining) break;
   }
-  const uint32_t T = prefix;   // the need-th largest key; `remaining` keys equal to T are taken
+  // Keys are compared on their resolved bits [low, 32): T is the need-th largest key's value
+  // there, and `remaining` keys with that value are taken (lowest index first).  When every
+  // bit is resolved this is the exact threshold key.
+  const uint32_t T = prefix >> low;
 
   // One scan of the packed counts (keys above T in the low half, keys equal to T in the high
   // half; each total is at most 8192) places every taken key: the equal keys are taken lowest
@@ -272,8 +281,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     const bool valid = i0 + j < n_c;
-    n_gt += valid && key[j] > T;
-    n_eq += valid && key[j] == T;
+    n_gt += valid && (key[j] >> low) > T;
+    n_eq += valid && (key[j] >> low) == T;
   }
   int tot;
   const int before = block_excl_scan(n_gt | (n_eq << 16), s_wave, &tot);
@@ -282,8 +291,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const SelectArgs
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     const bool valid = i0 + j < n_c;
-    bool take = valid && key[j] > T;
-    if (valid && key[j] == T) {
+    bool take = valid && (key[j] >> low) > T;
+    if (valid && (key[j] >> low) == T) {
       take = eq_rank < remaining;
       ++eq_rank;
     }

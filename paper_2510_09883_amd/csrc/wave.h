@@ -75,4 +75,13 @@ __device__ __forceinline__ uint32_t wave_and(uint32_t v) {
   return q[0] & q[1];
 }
 
+// Workgroup barrier that orders LDS accesses only: the waves wait for their own LDS operations,
+// not for outstanding global loads (which __syncthreads would also drain), so loads issued
+// before the barrier stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 }  // namespace delta
