@@ -2,10 +2,10 @@
 //
 // What it computes (Sec. 2, Eq. gqa_attention; App. A, Alg. 1): for sequence b and query
 // head j, out = sum_t softmax_t(scale * q_j . k_t) v_t over the rows of the sequence that the
-// mode selects, with k_t, v_t read from KV head j / G.  In Delta mode the scaled logits of
-// every token (group-major: [b][kv group][page][head in group][row]) and the per-head
-// log-sum-exp are also written, for the page scoring of
-// Sec. 4 ("Selection mechanism", "Page-based DELTA").
+// mode selects, with k_t, v_t read from KV head j / G.  With logits on (Delta layers) the
+// scaled logits of every token (group-major: [b][kv group][page][head in group][row]) and the
+// per-head log-sum-exp are also written, for the page scoring of Sec. 4 ("Selection
+// mechanism", "Page-based DELTA").
 //
 // Work decomposition.  One workgroup (4 waves) per (split, kv head g, sequence b).  A split
 // is a run of `gps` groups of 16 rows; a group is one 16-token page tile [16, D] of K and of
@@ -21,17 +21,16 @@
 //     probabilities and the per-head rescale factor go through a wave-private LDS slice;
 //   * P.V on the vector ALUs: each lane owns 8 consecutive head-dim columns of 16/RPI rows
 //     (128-bit loads, one V row per LPR consecutive lanes, fully coalesced).
-//   K/V of the next group are loaded before the current one is consumed (register double
-//   buffer) so every wave keeps 8 KB of loads in flight; waves interleave in blocks of four
-//   groups.  In Delta mode the logits of up to 2048/G groups are staged in LDS and written by
-//   the whole workgroup between chunks.
+//   Each wave keeps a ring of R register tiles: while one group is consumed, the K/V loads of
+//   the next R - 1 groups are in flight.  With logits on, the logits of a chunk of groups are
+//   staged in LDS and written by the whole workgroup between chunks.
 //
 // Split combine.  The 4 waves merge through LDS into one (max, sum, o) partial per split,
-// written to the workspace.  The last workgroup of each (b, g) to arrive (device-scope fence +
-// atomic counter) merges the partials in split order — a fixed order, so results do not
-// depend on arrival order — writes bf16 outputs (and the log-sum-exp), and re-arms the
-// counter to zero for the next launch.  A sequence that fits one split skips all of this and
-// writes its outputs directly.
+// written to the workspace with device-coherent stores.  The last workgroup of each (b, g) to
+// arrive (device-scope atomic counter) loads every split's partial at once into registers,
+// merges them in split order — a fixed order, so results do not depend on arrival order — writes bf16
+// outputs (and the log-sum-exp), and re-arms the counter to zero for the next launch.  A
+// sequence that fits one split skips all of this and writes its outputs directly.
 #include "internal.h"
 #include "wave.h"
 
@@ -41,9 +40,16 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = kAttnThreads / 64;
 constexpr float kNegInf = -__builtin_huge_valf();
+// Buffer-resource word 3 for raw (unformatted, stride 0) buffer access on gfx950, and the
+// cache-policy operand of the buffer builtins that selects the device-coherent (sc1) policy.
+constexpr int kRawBufferFlags = 0x00020000;
+constexpr int kCoherent = 16;
+// LDS floats for staging Delta-layer logits (64 KB: two Delta workgroups fit on a CU).
+constexpr int kStageFloats = 16384;
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -70,6 +76,8 @@ struct Geo {
   static constexpr int LPR = D / 8;     // lanes per V row
   static constexpr int RPI = 64 / LPR;  // V rows per wave-wide load
   static constexpr int NI = 16 / RPI;   // V loads per lane per group
+  // register tiles per wave: loads of R - 1 groups stay in flight while one is consumed
+  static constexpr int R = D == 128 ? 3 : 4;
 };
 
 template <int D>
@@ -79,9 +87,10 @@ struct Tile {
   uint32_t kmask;   // bit r: row r valid (rows of the MFMA A operand and of the score tile)
 };
 
-template <int D, int G, int MODE>
+template <int D, int G, int MODE, bool LOGITS>
 __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   using Gm = Geo<D>;
+  constexpr int R = Gm::R;
   const int split = blockIdx.x;
   const int g = blockIdx.y;
   const int b = blockIdx.z;
@@ -112,7 +121,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   const int cand = max(0, min(a.gps, a.max_groups - g0));
 
   __shared__ int s_rows[kMaxRowSlots];
-  __shared__ int s_aux[kMaxRowSlots];
+  __shared__ int s_aux[MODE == ROWS_SEL_PAGE ? kMaxRowSlots : 1];
   const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
   if (MODE == ROWS_DENSE) {
     for (int i = tid; i < cand; i += kAttnThreads) s_rows[i] = pt[g0 + i];
@@ -154,7 +163,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     if (split == 0) {
       for (int i = tid; i < G * D; i += kAttnThreads)
         a.out[((size_t)b * Hq + g * G) * D + i] = 0;
-      if (a.lse && tid < G) a.lse[(size_t)b * Hq + g * G + tid] = kNegInf;
+      if (LOGITS && tid < G) a.lse[(size_t)b * Hq + g * G + tid] = kNegInf;
     }
     return;
   }
@@ -163,7 +172,10 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   lds_barrier();   // the page / row list is in LDS; the query loads may still be in flight
 
   const size_t head_off = (size_t)g * 16 * D;
-  auto load_tile = [&](Tile<D>& t, int li) {
+  // Loads tile `li` of the split.  A prefetch past the wave's last group (real == false) is
+  // still issued, so that the loop's memory waits stay uniform, but with every lane at the
+  // tile's first 16 bytes: one cache line per load instruction instead of a whole tile.
+  auto load_tile = [&](Tile<D>& t, int li, bool real) {
     if (MODE == ROWS_SEL_TOKEN) {
       // every row is its own (page, row); rows past the selection re-read the group's first
       const int* rows = s_rows + 16 * li;
@@ -172,29 +184,30 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       t.kmask = 0;
 #pragma unroll
       for (int r = 0; r < 16; ++r) t.kmask |= ((rows[r] >= 0 && base + r < sel_n) ? 1u : 0u) << r;
-      int kr = ((t.kmask >> hcol) & 1u) ? rows[hcol] : first;
+      const int kr = ((t.kmask >> hcol) & 1u) && real ? rows[hcol] : first;
       const uint16_t* kp = a.k_cache + (size_t)(kr >> 4) * a.page_stride + head_off +
-                           (size_t)(kr & 15) * D + 8 * quad;
+                           (size_t)(kr & 15) * D + (real ? 8 * quad : 0);
 #pragma unroll
-      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
+      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + (real ? 32 * ks : 0));
 #pragma unroll
       for (int i = 0; i < Gm::NI; ++i) {
         const int r = Gm::RPI * i + lane / Gm::LPR;
-        const int vr = ((t.kmask >> r) & 1u) ? rows[r] : first;
+        const int vr = ((t.kmask >> r) & 1u) && real ? rows[r] : first;
         t.v[i] = load16(a.v_cache + (size_t)(vr >> 4) * a.page_stride + head_off +
-                        (size_t)(vr & 15) * D + 8 * (lane % Gm::LPR));
+                        (size_t)(vr & 15) * D + (real ? 8 * (lane % Gm::LPR) : 0));
       }
     } else {
       const size_t page = (size_t)s_rows[li] * a.page_stride + head_off;
       const int unit = (MODE == ROWS_DENSE) ? g0 + li : s_aux[li];
       const int nrows = min(16, s_b - 16 * unit);
       t.kmask = (nrows >= 16) ? 0xffffu : ((1u << max(nrows, 0)) - 1u);
-      const uint16_t* kp = a.k_cache + page + (size_t)hcol * D + 8 * quad;
+      const uint16_t* kp = a.k_cache + page + (real ? (size_t)hcol * D + 8 * quad : 0);
 #pragma unroll
-      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + 32 * ks);
-      const uint16_t* vp = a.v_cache + page + (size_t)(lane / Gm::LPR) * D + 8 * (lane % Gm::LPR);
+      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16(kp + (real ? 32 * ks : 0));
+      const uint16_t* vp = a.v_cache + page +
+                           (real ? (size_t)(lane / Gm::LPR) * D + 8 * (lane % Gm::LPR) : 0);
 #pragma unroll
-      for (int i = 0; i < Gm::NI; ++i) t.v[i] = load16(vp + (size_t)Gm::RPI * i * D);
+      for (int i = 0; i < Gm::NI; ++i) t.v[i] = load16(vp + (real ? (size_t)Gm::RPI * i * D : 0));
     }
   };
 
@@ -210,16 +223,14 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
 
   const int Hq_row = b * Hq + g * G;
-  // Delta mode: the workgroup keeps the logits of a chunk of kChunk groups in LDS
-  // ([group][head][16], the global layout; about 128 KB) and writes the chunk out
-  // cooperatively between chunks, with non-temporal (streaming) stores.  Measured on MI355X,
-  // logit stores interleaved with the K/V read stream cost several times their bytes, while
-  // the same bytes written in a few large streaming bursts (reads paused) cost about their
-  // share; so chunks are as large as LDS allows.
-  constexpr int kChunk = (2048 / G) / 16 * 16;             // a multiple of 16
-  __shared__ __attribute__((aligned(16))) float s_stage[MODE == ROWS_DENSE ? kChunk * G * 16 : 1];
-  const bool want_logits = MODE == ROWS_DENSE && a.logits != nullptr;
-  auto process = [&](const Tile<D>& t, int li, int slot) {
+  // Logits on: the workgroup keeps the logits of a chunk of kChunk groups in LDS ([group]
+  // [head][16], the global layout) and writes the chunk out cooperatively between chunks, with
+  // non-temporal (streaming) stores.  Measured on MI355X, logit stores interleaved with the
+  // K/V read stream cost several times their bytes, while the same bytes written in a few large
+  // streaming bursts (reads paused) cost about their share.  A chunk is a multiple of 16 groups.
+  constexpr int kChunk = (kStageFloats / (G * 16)) / 16 * 16;
+  __shared__ __attribute__((aligned(16))) float s_stage[LOGITS ? kChunk * G * 16 : 1];
+  auto process = [&](const Tile<D>& t, int slot) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < Gm::NK; ++ks)
@@ -229,7 +240,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
-    if (want_logits && hcol < G)
+    if (LOGITS && hcol < G)
       *reinterpret_cast<f32x4*>(s_stage + (slot * G + hcol) * 16 + 4 * quad) = f32x4{x[0], x[1], x[2], x[3]};
     float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
     mx = max_xor32(max_xor16(mx));
@@ -284,33 +295,44 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   };
 
   // Waves interleave in blocks of four groups (wave w takes groups 16j + 4w .. 16j + 4w + 3),
-  // so the workgroup streams about sixteen adjacent pages at a time.  Register double buffer:
-  // the next group's K/V loads are in flight while the current group is consumed; the
-  // prefetch past the wave's last group is clamped to that group (already requested: served
-  // by the caches).  The chunk loop is uniform over the workgroup (its barriers are reached by
-  // every wave); without logits there is a single chunk.
+  // so the workgroup streams about sixteen adjacent pages at a time.  A wave walks its groups
+  // [kb, ke) with a ring of R register tiles: tile k lives in slot k % R, and while it is
+  // consumed the loads of tiles k + 1 .. k + R - 1 are in flight.  Every load is issued
+  // unconditionally (a prefetch past ke is a one-line dummy read of the range's last group)
+  // and the loop has no other exits, so the compiler's wait for tile k never drains the
+  // younger loads.  With logits on, the groups are walked in chunks with the ring drained at
+  // each chunk end; the chunk loop is uniform over the workgroup (its barriers are reached by
+  // every wave).
   {
     auto group_of = [&](int k) { return 16 * (k >> 2) + 4 * wave + (k & 3); };
     const int full_blocks = ng / 16, rem = ng - 16 * full_blocks;
     const int n_mine = 4 * full_blocks + min(4, max(0, rem - 4 * wave));
-    const int last = n_mine > 0 ? group_of(n_mine - 1) : 0;
-    const int chunk = want_logits ? kChunk : ng;
-    Tile<D> cur, nxt;
-    if (n_mine > 0) load_tile(cur, group_of(0));
-    int k = 0;
-    for (int c0 = 0; c0 < ng; c0 += chunk) {
-      // this wave's groups below c0 + chunk (all remaining ones in the last chunk)
-      const int kend = c0 + chunk >= ng ? n_mine : min(n_mine, ((c0 + chunk) / 16) * 4);
-      for (; k < kend; ++k) {
-        const int li = group_of(k);
-        load_tile(nxt, k + 1 < n_mine ? group_of(k + 1) : last);
-        process(cur, li, li - c0);
-        cur = nxt;
+    auto walk = [&](int kb, int ke, int c0) {
+      if (kb >= ke) return;
+      auto fetch = [&](Tile<D>& t, int k) { load_tile(t, group_of(min(k, ke - 1)), k < ke); };
+      Tile<D> t[R];
+#pragma unroll
+      for (int i = 0; i < R - 1; ++i) fetch(t[i], kb + i);
+      for (int k = kb; k < ke; k += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          fetch(t[(r + R - 1) % R], k + r + R - 1);
+          if (k + r < ke) process(t[r], group_of(k + r) - c0);
+        }
       }
-      if (want_logits) {
+    };
+    if (!LOGITS) {
+      walk(0, n_mine, 0);
+    } else {
+      for (int c0 = 0; c0 < ng; c0 += kChunk) {
+        // this wave's groups in [c0, c0 + kChunk): a whole number of blocks of 16 except in
+        // the last chunk
+        const int kb = (c0 / 16) * 4;
+        const int ke = min(n_mine, ((c0 + kChunk) / 16) * 4);
+        walk(kb, ke, c0);
         // chunk [c0, c0 + n) goes to [b][kv group][page g0 + c0 ...][head][16], contiguous
         lds_barrier();
-        const int n = min(chunk, ng - c0) * G * 16;
+        const int n = min(kChunk, ng - c0) * G * 16;
         float* dst = a.logits + (((size_t)b * a.n_kv_heads + g) * a.logit_pages + g0 + c0) * G * 16;
         for (int i = 4 * tid; i < n; i += 4 * kAttnThreads)
           __builtin_nontemporal_store(*reinterpret_cast<const f32x4*>(s_stage + i),
@@ -371,7 +393,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     packed.x = (uint32_t)f32_to_bf16_rne(v[0] / lsum) | ((uint32_t)f32_to_bf16_rne(v[1] / lsum) << 16);
     packed.y = (uint32_t)f32_to_bf16_rne(v[2] / lsum) | ((uint32_t)f32_to_bf16_rne(v[3] / lsum) << 16);
     *reinterpret_cast<uint2*>(a.out + (size_t)(Hq_row + h) * D + dc) = packed;
-    if (dc == 0 && a.lse) a.lse[(size_t)Hq_row + h] = mx + log2f(lsum);
+    if (LOGITS && dc == 0) a.lse[(size_t)Hq_row + h] = mx + log2f(lsum);
   };
 
   // A sequence with a single split needs no combine: the workgroup writes the output itself.
@@ -380,77 +402,89 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     return;
   }
 
-  const size_t pbase = ((size_t)bg * a.n_split + split) * G;
+  // ---- split combine --------------------------------------------------------------------
+  // Partials are written and read only with device-coherent accesses (the sc1 cache policy:
+  // written through to memory, and read past any stale copy in another XCD's L2), so no L2
+  // write-back or invalidation is needed to publish them.  Each thread waits until its partial
+  // stores are complete, the barrier makes that true for the whole workgroup, and only then
+  // does one thread count the workgroup in with a device-scope atomic; the workgroup that
+  // brings the count to n_valid reads every partial after the atomic has returned.  (A
+  // release/acquire fence pair would instead write back and invalidate the whole L2 of the
+  // XCD once per workgroup; measured on MI355X that serialises launches of many workgroups.)
+  const int pair_floats = a.n_split * G * D;
+  const __amdgpu_buffer_rsrc_t po = __builtin_amdgcn_make_buffer_rsrc(
+      a.part_o + (size_t)bg * pair_floats, 0, pair_floats * 4, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t pml = __builtin_amdgcn_make_buffer_rsrc(
+      a.part_ml + (size_t)bg * a.n_split * G * 2, 0, a.n_split * G * 8, kRawBufferFlags);
+  const int o_off = (h * D + dc) * 4;   // this thread's bytes inside one split's G x D block
   if (owner) {
-    *reinterpret_cast<f32x4*>(a.part_o + (pbase + h) * D + dc) = O;
-    if (dc == 0) *reinterpret_cast<float2*>(a.part_ml + (pbase + h) * 2) = make_float2(M, L);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, O), po, o_off,
+                                           split * G * D * 4, kCoherent);
+    if (dc == 0)
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, make_float2(M, L)), pml,
+                                            h * 8, split * G * 8, kCoherent);
   }
-
-  // ---- last workgroup of (b, g) merges the splits -----------------------------------------
-  // Every thread waits for its partial stores to complete; after the barrier one thread
-  // publishes the workgroup's partial with a device-scope release and counts it in.  The
-  // workgroup that brings the count to n_valid acquires (device scope) before reading the
-  // other workgroups' partials.  One release per workgroup keeps the cache write-back cost low.
-  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores are complete
   __syncthreads();
   __shared__ int s_last;
   if (tid == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     const int prev = __hip_atomic_fetch_add(&a.counters[bg], 1, __ATOMIC_RELAXED,
                                             __HIP_MEMORY_SCOPE_AGENT);
     s_last = prev == n_valid - 1;
-    if (s_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!s_last || !owner) return;
 
-  // The split (max, sum) pairs go to LDS while the first batch of the thread's partial outputs
-  // is already being loaded (one wait for memory when n_valid <= kMergeBatch); each thread then
-  // derives its head's max and weights from LDS itself.  Splits are summed in split order: the
-  // result does not depend on the order in which workgroups finished.
+  // Every owner thread loads its head's (max, sum) and its four outputs of kMergeBatch splits
+  // at once (one wait for memory per batch, a single batch up to kMergeBatch splits) and folds
+  // them into a running (max, sum, o) in split order: the result does not depend on the order
+  // in which workgroups finished.
   constexpr int kMergeBatch = 16;
-  __shared__ __attribute__((aligned(16))) float2 s_ml[kMaxSplits * kMaxGroup];
-  const size_t cbase = (size_t)bg * a.n_split * G;
-  for (int i = tid; i < n_valid * G; i += kAttnThreads)
-    s_ml[i] = *reinterpret_cast<const float2*>(a.part_ml + (cbase + i) * 2);
-  f32x4 pv[kMergeBatch];
-  auto load_batch = [&](int c0) {
-#pragma unroll
-    for (int c = 0; c < kMergeBatch; ++c) {
-      const int cc = min(c0 + c, n_valid - 1);
-      pv[c] = *reinterpret_cast<const f32x4*>(a.part_o + (cbase + (size_t)cc * G + h) * D + dc);
-    }
-  };
-  if (owner) load_batch(0);
-  lds_barrier();   // s_ml is in LDS; the partial outputs may still be arriving
-  if (!owner) return;
   M = kNegInf;
-  for (int c = 0; c < n_valid; ++c) M = fmaxf(M, s_ml[c * G + h].x);
   L = 0.f;
   O = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < n_valid; c0 += kMergeBatch) {
-    if (c0 > 0) load_batch(c0);
+    float2 ml[kMergeBatch];
+    f32x4 pv[kMergeBatch];
+#pragma unroll
+    for (int c = 0; c < kMergeBatch; ++c) {
+      const int cc = min(c0 + c, n_valid - 1);
+      ml[c] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(pml, h * 8, cc * G * 8, kCoherent));
+      pv[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(po, o_off, cc * G * D * 4, kCoherent));
+    }
+    float bm = kNegInf;
+#pragma unroll
+    for (int c = 0; c < kMergeBatch; ++c)
+      if (c0 + c < n_valid) bm = fmaxf(bm, ml[c].x);
+    const float Mn = fmaxf(M, bm);
+    const float Mu = (Mn == kNegInf) ? 0.f : Mn;
+    const float rs = exp2f(M - Mu);   // 0 while nothing has been folded in (M = -inf)
+    L *= rs;
+    O *= rs;
 #pragma unroll
     for (int c = 0; c < kMergeBatch; ++c) {
       if (c0 + c < n_valid) {
-        const float2 ml = s_ml[(c0 + c) * G + h];
-        const float f = (ml.x == kNegInf) ? 0.f : exp2f(ml.x - M);
-        L += f * ml.y;
+        const float f = (ml[c].x == kNegInf) ? 0.f : exp2f(ml[c].x - Mu);
+        L += f * ml[c].y;
         O += f * pv[c];
       }
     }
+    M = Mn;
   }
   store_out(O, L, M);
-  if (tid == 0) a.counters[bg] = 0;
+  if (tid == 0) __hip_atomic_store(&a.counters[bg], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int D, int G>
 hipError_t launch_dg(int mode, const AttnArgs& a, int batch, hipStream_t stream) {
   const dim3 grid(a.n_split, a.n_kv_heads, batch), block(kAttnThreads);
   switch (mode) {
-    case ROWS_DENSE: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_DENSE>), grid, block, 0, stream, a); break;
-    case ROWS_SEL_PAGE: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_PAGE>), grid, block, 0, stream, a); break;
-    case ROWS_SEL_TOKEN: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_TOKEN>), grid, block, 0, stream, a); break;
+    case ROWS_DENSE:
+      if (a.logits) hipLaunchKernelGGL((attn_kernel<D, G, ROWS_DENSE, true>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((attn_kernel<D, G, ROWS_DENSE, false>), grid, block, 0, stream, a);
+      break;
+    case ROWS_SEL_PAGE: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_PAGE, false>), grid, block, 0, stream, a); break;
+    case ROWS_SEL_TOKEN: hipLaunchKernelGGL((attn_kernel<D, G, ROWS_SEL_TOKEN, false>), grid, block, 0, stream, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
