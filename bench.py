@@ -346,7 +346,8 @@ def main():
     kernel_name = {"full": "attn_kernel (dense rows)", "delta": "attn_kernel + score + select",
                    "sparse": "attn_kernel (selected pages)"}[dominant]
     mode = {"full": 0, "delta": 0, "sparse": 1 if w.unit_tokens == 16 else 2}[dominant]
-    kernel_tag = f"attn_kernel<{w.head_dim}, {w.group}, {mode}>"
+    logits = "true" if dominant == "delta" else "false"
+    kernel_tag = f"attn_kernel<{w.head_dim}, {w.group}, {mode}, {logits}>"
     traffic = measured_traffic(dominant, w, kernel_tag)
     achieved = role_bytes[dominant] / (layer_us[dominant] * 1e-6) / 1e9
     overhead = (layer_us["delta"] - layer_us["full"]) / layer_us["full"] if "delta" in layer_us and "full" in layer_us else None
