@@ -48,8 +48,9 @@ constexpr float kNegInf = -__builtin_huge_valf();
 // cache-policy operand of the buffer builtins that selects the device-coherent (sc1) policy.
 constexpr int kRawBufferFlags = 0x00020000;
 constexpr int kCoherent = 16;
-// LDS floats for staging Delta-layer logits (64 KB: two Delta workgroups fit on a CU).
-constexpr int kStageFloats = 16384;
+// LDS floats for staging Delta-layer logits (128 KB: one Delta workgroup per CU; measured on
+// MI355X, fewer and larger chunk flushes beat two resident workgroups with half the staging).
+constexpr int kStageFloats = 32768;
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);

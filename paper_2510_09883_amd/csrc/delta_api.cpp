@@ -22,10 +22,10 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Workgroups the attention launch aims for: about one per CU (256 CUs).  Fewer, longer
-// workgroups keep the number of device-scope releases of the split combine low (each one
-// writes back the XCD's L2), which measured faster than more, shorter workgroups at every
-// workload size.  DELTA_ATTN_TARGET_WGS overrides it for tuning.
+// Workgroups the attention launch aims for: about one per CU (256 CUs).  Measured on MI355X,
+// more and shorter workgroups (up to 4096) were slower at every workload size: each one pays a
+// dependent metadata load, an LDS wave merge and a partial store before its work is counted.
+// DELTA_ATTN_TARGET_WGS overrides it for tuning.
 int target_workgroups() {
   static int v = [] {
     const char* e = getenv("DELTA_ATTN_TARGET_WGS");
@@ -48,9 +48,9 @@ int min_groups_per_split() {
 }
 
 // Most splits per (sequence, kv head).  The last workgroup's merge reads every split's partial
-// and each split adds a device-scope release and an arrival to the same counter, so beyond ~16
-// splits the combine costs more than the shorter loop saves (measured on MI355X with one
-// sequence of 8K tokens).  DELTA_ATTN_MAX_SPLITS overrides it for tuning.
+// (one batch of loads per 16 splits) and each split adds an arrival on the same counter, so
+// beyond ~16 splits the combine costs more than the shorter loop saves (measured on MI355X with
+// one sequence of 8K tokens).  DELTA_ATTN_MAX_SPLITS overrides it for tuning.
 int max_splits() {
   static int v = [] {
     const char* e = getenv("DELTA_ATTN_MAX_SPLITS");
