@@ -31,7 +31,8 @@
  *   Numerics. bf16 inputs, fp32 accumulation and online softmax, bf16 round-to-nearest-even
  *             outputs.  Results are deterministic: the same inputs and shape give bitwise
  *             identical outputs, and a DELTA layer's attention output is bitwise identical to
- *             delta_full_attn's on the same inputs.
+ *             delta_full_attn's on the same inputs (with the optional fused DELTA kernel, see
+ *             delta_delta_attn_select, the two agree up to floating-point summation order).
  *   Workspace. `ws` is caller-owned device memory of at least delta_workspace_bytes() bytes.
  *             It must be zero-filled once after allocation; every call leaves it ready for the
  *             next call.  Calls that share one workspace must not run concurrently.
@@ -121,7 +122,12 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  *                every sparse layer that shares this page table the page-table lookup.
  *                NULL: not written.
  *   unit_scores: optional fp32 [B, ceil(max_seq_len / U)]: S_u for u < ceil(seq_lens[b]/U);
- *                NULL keeps them in the workspace. */
+ *                NULL keeps them in the workspace.
+ * Launches: the attention kernel (which stages the logits through the workspace), a scoring
+ * kernel and a selection kernel.  With DELTA_DELTA_PATH=fused in the environment, shapes with
+ * head_dim 128, a multiple of 4 KV heads, at most 32 query heads and at most 2048 candidate
+ * units instead run one cooperative kernel that keeps the logits on chip (opt-in: on MI355X its
+ * cooperative launch costs more than the logit traffic it saves). */
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
                             int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,

@@ -31,19 +31,15 @@
 // merges them in split order — a fixed order, so results do not depend on arrival order — writes bf16
 // outputs (and the log-sum-exp), and re-arms the counter to zero for the next launch.  A
 // sequence that fits one split skips all of this and writes its outputs directly.
+#include "attn_tile.h"
 #include "internal.h"
 #include "wave.h"
 
 namespace delta {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
 constexpr int kWaves = kAttnThreads / 64;
-constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kNegInf = kNegInfF;
 // Buffer-resource word 3 for raw (unformatted, stride 0) buffer access on gfx950, and the
 // cache-policy operand of the buffer builtins that selects the device-coherent (sc1) policy.
 constexpr int kRawBufferFlags = 0x00020000;
@@ -51,47 +47,6 @@ constexpr int kCoherent = 16;
 // LDS floats for staging Delta-layer logits (128 KB: one Delta workgroup per CU; measured on
 // MI355X, fewer and larger chunk flushes beat two resident workgroups with half the staging).
 constexpr int kStageFloats = 32768;
-
-__device__ __forceinline__ u32x4 load16(const uint16_t* p) {
-  return *reinterpret_cast<const u32x4*>(p);
-}
-// K/V rows are read once per launch: non-temporal loads.  Measured on MI355X they raise the
-// streaming rate of the full and sparse layers by 5-20 % over ordinary loads.
-__device__ __forceinline__ u32x4 load16_stream(const uint16_t* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
-
-// Compiler-level ordering for LDS traffic that stays inside one wave (the LDS unit executes
-// one wave's requests in order; this only stops the compiler from moving them).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-template <int D>
-struct Geo {
-  static constexpr int NK = D / 32;     // MFMA k-steps = 16-byte K loads per lane per group
-  static constexpr int LPR = D / 8;     // lanes per V row
-  static constexpr int RPI = 64 / LPR;  // V rows per wave-wide load
-  static constexpr int NI = 16 / RPI;   // V loads per lane per group
-  // register tiles per wave: loads of R - 1 groups stay in flight while one is consumed
-  static constexpr int R = D == 128 ? 3 : 4;
-};
-
-template <int D>
-struct Tile {
-  u32x4 k[Geo<D>::NK];
-  u32x4 v[Geo<D>::NI];
-  uint32_t kmask;   // bit r: row r valid (rows of the MFMA A operand and of the score tile)
-};
 
 template <int D, int G, int MODE, bool LOGITS>
 __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
@@ -112,15 +67,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   // page (or row) list are all requested at once; the list is staged in LDS speculatively
   // (bounded by the host's group bound) and trimmed once the length is known.
   bf16x8 qb[Gm::NK];
-  {
-    const uint16_t* qp = a.q + ((size_t)b * Hq + g * G + min(hcol, G - 1)) * D + 8 * quad;
-#pragma unroll
-    for (int ks = 0; ks < Gm::NK; ++ks) {
-      u32x4 w = load16(qp + 32 * ks);
-      if (hcol >= G) w = u32x4{0u, 0u, 0u, 0u};
-      qb[ks] = __builtin_bit_cast(bf16x8, w);
-    }
-  }
+  load_query<D, G>(qb, a.q, (size_t)b * Hq + g * G, lane);
   const int s_b = a.seq_lens[b];
   const int sel_n = (MODE == ROWS_DENSE) ? 0 : min(a.sel_cnt[b], a.sel_stride);
   const int g0 = split * a.gps;
@@ -207,13 +154,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       const int unit = (MODE == ROWS_DENSE) ? g0 + li : s_aux[li];
       const int nrows = min(16, s_b - 16 * unit);
       t.kmask = (nrows >= 16) ? 0xffffu : ((1u << max(nrows, 0)) - 1u);
-      const uint16_t* kp = a.k_cache + page + (real ? (size_t)hcol * D + 8 * quad : 0);
-#pragma unroll
-      for (int ks = 0; ks < Gm::NK; ++ks) t.k[ks] = load16_stream(kp + (real ? 32 * ks : 0));
-      const uint16_t* vp = a.v_cache + page +
-                           (real ? (size_t)(lane / Gm::LPR) * D + 8 * (lane % Gm::LPR) : 0);
-#pragma unroll
-      for (int i = 0; i < Gm::NI; ++i) t.v[i] = load16_stream(vp + (real ? (size_t)Gm::RPI * i * D : 0));
+      load_page_tile<D>(t, a.k_cache + page, a.v_cache + page, real, lane);
     }
   };
 
@@ -221,12 +162,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   __shared__ float s_p[kWaves][16 * 8 + 8];
   float* lp = s_p[wave];
 
-  float m_run = kNegInf, l_run = 0.f;   // per head hcol (valid for hcol < G)
-  float o[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+  WaveSoftmax<G> st;
+  st.init();
 
   const int Hq_row = b * Hq + g * G;
   // Logits on: the workgroup keeps the logits of a chunk of kChunk groups in LDS ([group]
@@ -237,67 +174,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   constexpr int kChunk = (kStageFloats / (G * 16)) / 16 * 16;
   __shared__ __attribute__((aligned(16))) float s_stage[LOGITS ? kChunk * G * 16 : 1];
   auto process = [&](const Tile<D>& t, int slot) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < Gm::NK; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.k[ks]), qb[ks],
-                                                    acc, 0, 0, 0);
-    float x[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      x[r] = ((t.kmask >> (4 * quad + r)) & 1u) ? acc[r] * a.scale_log2 : kNegInf;
-    if (LOGITS && hcol < G)
-      *reinterpret_cast<f32x4*>(s_stage + (slot * G + hcol) * 16 + 4 * quad) = f32x4{x[0], x[1], x[2], x[3]};
-    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mx = max_xor32(max_xor16(mx));
-    const float m_new = fmaxf(m_run, mx);
-    // m_new is finite whenever the group has a valid row (always, for valid selections); the
-    // guard keeps an all-masked group from turning the running state into NaN
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
-    float p[4], ps = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      p[r] = exp2f(x[r] - m_use);
-      ps += p[r];
-    }
-    ps = sum_xor32(sum_xor16(ps));
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-
-    wave_lds_sync();
-    if (hcol < G) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) lp[(4 * quad + r) * 8 + hcol] = p[r];
-      if (quad == 0) lp[128 + hcol] = alpha;
-    }
-    wave_lds_sync();
-
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float al = lp[128 + h];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] *= al;
-    }
-#pragma unroll
-    for (int i = 0; i < Gm::NI; ++i) {
-      const int row = Gm::RPI * i + lane / Gm::LPR;
-      u32x4 w = t.v[i];
-      if (!((t.kmask >> row) & 1u)) w = u32x4{0u, 0u, 0u, 0u};   // rows past the end may hold NaN
-      float v[8];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        v[2 * c] = __uint_as_float(w[c] << 16);
-        v[2 * c + 1] = __uint_as_float(w[c] & 0xffff0000u);
-      }
-      const float* pr = lp + row * 8;
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float ph = pr[h];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph, v[e], o[h][e]);
-      }
-    }
+    process_tile<D, G, LOGITS>(t, qb, a.scale_log2, st, lp, s_stage + slot * G * 16, lane);
   };
 
   // Waves interleave in blocks of four groups (wave w takes groups 16j + 4w .. 16j + 4w + 3),
@@ -349,28 +226,21 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   }
 
   // ---- reduce o over the lanes that share a head-dim chunk -------------------------------
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = o[h][e];
-      if (Gm::LPR == 8) v += lane_xor8(v);
-      o[h][e] = sum_xor32(sum_xor16(v));
-    }
+  reduce_outputs<D, G>(st);
 
   // ---- merge the 4 waves into one split partial ------------------------------------------
   __shared__ float s_m[kWaves][kMaxGroup], s_l[kWaves][kMaxGroup];
   __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][D];
   static_assert(G * D <= 4 * kAttnThreads && D % 4 == 0, "four outputs per thread cover a group");
   if (quad == 0 && hcol < G) {
-    s_m[wave][hcol] = m_run;
-    s_l[wave][hcol] = l_run;
+    s_m[wave][hcol] = st.m_run;
+    s_l[wave][hcol] = st.l_run;
   }
   if (lane < Gm::LPR) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s_o[wave][h][8 * lane + e] = o[h][e];
+      for (int e = 0; e < 8; ++e) s_o[wave][h][8 * lane + e] = st.o[h][e];
   }
   lds_barrier();
 

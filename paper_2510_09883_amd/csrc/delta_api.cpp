@@ -7,6 +7,7 @@
 // counts on the device, so no step needs a device-to-host round trip.
 #include <math.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include <algorithm>
 
@@ -86,7 +87,9 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
 
 struct Layout {
   size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, phys = 0;
+  size_t fcnt = 0;
   size_t total = 0;
+  int fused_chunks = 0;   // chunks per sequence of the fused Delta kernel
   int max_split = 0;
   int logit_pages = 0;
   int nu_stride = 0;
@@ -146,16 +149,23 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
       return DELTA_ERR_UNSUPPORTED;
   }
   L->logit_pages = ceil_div(s->max_seq_len, 16);
+  // partial rows per (sequence, KV head): the split plan's, or the fused Delta kernel's chunks
+  int part_splits = L->max_split;
+  if (sel) {
+    L->fused_chunks = ceil_div(L->logit_pages, kFusedChunkPages);
+    part_splits = std::max(part_splits, L->fused_chunks);
+  }
   size_t off = 0;
   L->counters = off;  off = align_up(off + sizeof(int32_t) * pairs);
-  L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * 2);
-  L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * L->max_split * G * s->head_dim);
+  L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * 2);
+  L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * s->head_dim);
   if (sel) {
     L->nu_stride = ceil_div(s->max_seq_len, sel->unit_tokens);
     L->logits = off;  off = align_up(off + sizeof(float) * (size_t)s->batch * L->logit_pages * s->n_q_heads * 16);
     L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
     L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
     L->phys = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * (sel->budget_tokens / sel->unit_tokens));
+    L->fcnt = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * 2);
   }
   L->total = off;
   return DELTA_OK;
@@ -207,29 +217,43 @@ int run_full(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* 
 
 // `phys` (nullable): where the select kernel also writes the physical location of every
 // selected unit, read through this layer's page table.
+// Whether a Delta layer runs as one fused cooperative launch (logits kept in LDS) instead of
+// attention + scoring + selection launches.  The fused kernel needs head_dim 128, a multiple of
+// 4 KV heads, at most kFusedMaxQHeads query heads, at most 2048 selection candidates, and a grid
+// of (chunks x sequences) that the device keeps resident at once.  It is used only when
+// DELTA_DELTA_PATH=fused is set in the environment: measured on MI355X (Qwen-7B shape, 8 x 32K)
+// a cooperative launch costs about 17 us more than a plain one, and the fused layer took 124 us
+// against 114 us for the split path (107 us with a plain launch, which cannot guarantee the
+// co-residency its sequence barrier needs).
+bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const Layout& L) {
+  const char* e = getenv("DELTA_DELTA_PATH");
+  if (!e || strcmp(e, "fused")) return false;
+  const int G = s->n_q_heads / s->n_kv_heads;
+  if (s->head_dim != 128 || s->n_kv_heads % 4 != 0 || s->n_q_heads > kFusedMaxQHeads) return false;
+  const int n_c = L.nu_stride - sel->recent_tokens / sel->unit_tokens;
+  if (n_c > kFusedKeysPerThread * 256) return false;
+  const int64_t grid = (int64_t)L.fused_chunks * s->batch;
+  const int64_t part_bytes = (int64_t)s->batch * s->n_q_heads * L.fused_chunks * s->head_dim * 4;
+  if (part_bytes > 0x7fffffff) return false;
+  // capacity per device, group size and unit size, measured once
+  static int cache[64][kMaxGroup + 1][2];
+  static bool filled[64][kMaxGroup + 1][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  const int ui = sel->unit_tokens == 16 ? 0 : 1;
+  if (!filled[dev][G][ui]) {
+    cache[dev][G][ui] = fused_delta_capacity(s->head_dim, G, sel->unit_tokens);
+    filled[dev][G][ui] = true;
+  }
+  const int cap = cache[dev][G][ui];
+  return grid <= cap;
+}
+
 int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
               const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, float* uscores,
               int32_t* phys, const Layout& L, char* ws, hipStream_t st) {
-  AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
-  a.logits = reinterpret_cast<float*>(ws + L.logits);
-  a.lse = reinterpret_cast<float*>(ws + L.lse);
-  int rc = hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, ROWS_DENSE, a,
-                                   s->batch, st));
-  if (rc) return rc;
-  ScoreArgs sa{};
-  sa.logits = a.logits;
-  sa.lse = a.lse;
-  sa.seq_lens = kv->seq_lens;
-  sa.unit_scores = uscores ? uscores : reinterpret_cast<float*>(ws + L.uscores);
-  sa.n_q_heads = s->n_q_heads;
-  sa.n_kv_heads = s->n_kv_heads;
-  sa.logit_pages = L.logit_pages;
-  sa.nu_stride = L.nu_stride;
-  sa.max_seq_len = s->max_seq_len;
-  rc = hip_rc(launch_score(sel->agg, sel->unit_tokens, sa, s->batch, st));
-  if (rc) return rc;
   SelectArgs xa{};
-  xa.unit_scores = sa.unit_scores;
+  xa.unit_scores = uscores ? uscores : reinterpret_cast<float*>(ws + L.uscores);
   xa.seq_lens = kv->seq_lens;
   xa.page_table = kv->page_table;
   xa.sel_idx = sel_idx;
@@ -240,6 +264,47 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   xa.unit_tokens = sel->unit_tokens;
   xa.budget_units = sel->budget_tokens / sel->unit_tokens;
   xa.recent_units = sel->recent_tokens / sel->unit_tokens;
+  if (use_fused_delta(s, sel, L)) {
+    FusedArgs f{};
+    f.k_cache = static_cast<const uint16_t*>(kv->k_cache);
+    f.v_cache = static_cast<const uint16_t*>(kv->v_cache);
+    f.page_table = kv->page_table;
+    f.seq_lens = kv->seq_lens;
+    f.q = static_cast<const uint16_t*>(q);
+    f.out = static_cast<uint16_t*>(out);
+    f.part_o = reinterpret_cast<float*>(ws + L.part_o);
+    f.part_ml = reinterpret_cast<float*>(ws + L.part_ml);
+    f.counters = reinterpret_cast<int32_t*>(ws + L.fcnt);
+    f.unit_scores = const_cast<float*>(xa.unit_scores);
+    f.page_stride = (int64_t)s->n_kv_heads * 16 * s->head_dim;
+    f.n_q_heads = s->n_q_heads;
+    f.n_kv_heads = s->n_kv_heads;
+    f.max_pages = s->max_pages_per_seq;
+    f.n_chunks = L.fused_chunks;
+    f.max_seq_len = s->max_seq_len;
+    f.agg = sel->agg;
+    f.scale_log2 = scale_log2(s);
+    f.sel = xa;
+    return hip_rc(launch_fused_delta(s->head_dim, s->n_q_heads / s->n_kv_heads, f, s->batch, st));
+  }
+  AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
+  a.logits = reinterpret_cast<float*>(ws + L.logits);
+  a.lse = reinterpret_cast<float*>(ws + L.lse);
+  int rc = hip_rc(launch_attention(s->head_dim, s->n_q_heads / s->n_kv_heads, ROWS_DENSE, a,
+                                   s->batch, st));
+  if (rc) return rc;
+  ScoreArgs sa{};
+  sa.logits = a.logits;
+  sa.lse = a.lse;
+  sa.seq_lens = kv->seq_lens;
+  sa.unit_scores = const_cast<float*>(xa.unit_scores);
+  sa.n_q_heads = s->n_q_heads;
+  sa.n_kv_heads = s->n_kv_heads;
+  sa.logit_pages = L.logit_pages;
+  sa.nu_stride = L.nu_stride;
+  sa.max_seq_len = s->max_seq_len;
+  rc = hip_rc(launch_score(sel->agg, sel->unit_tokens, sa, s->batch, st));
+  if (rc) return rc;
   return hip_rc(launch_select(xa, s->batch, st));
 }
 

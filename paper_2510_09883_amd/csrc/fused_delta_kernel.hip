@@ -1,0 +1,295 @@
+// Fused Delta layer for gfx950: full attention, token/page scoring and page selection of one
+// Delta layer (App. A, Alg. 1 Delta branch and Alg. 2 RefreshPages; Sec. 4 "Selection
+// mechanism", "Page-based DELTA") in one cooperative launch, with the logits kept in LDS.
+//
+// One workgroup per (chunk of kFusedChunkPages pages, sequence) covers every KV head of the
+// chunk: wave w takes KV heads w, w + 4, ... and walks the chunk's pages with the register
+// tile ring of the split attention kernel, putting every scaled log2-domain logit into LDS
+// ([kv head][page][head in group][16]).  Then:
+//   1. each wave stores its chunk partial (max, sum, o) per query head (device-coherent);
+//   2. the workgroups of a sequence wait for each other (device-scope counter; the cooperative
+//      launch guarantees that all of them are resident);
+//   3. every workgroup forms the log-sum-exp of all query heads from the chunk partials;
+//   4. workgroup c merges the outputs of heads c, c + n_chunks, ... in chunk order;
+//   5. every workgroup scores its own tokens from its LDS logits, s_t = 2^(max_j (x_j(t) -
+//      lse_j)) (or sum_j 2^(x_j(t) - lse_j)), sums them per page and stores the page scores;
+//   6. the last workgroup of the sequence to finish scoring selects for it (select_impl.h).
+// The logits never reach HBM; the split path (attention kernel + score kernel + select
+// kernel) writes and re-reads them.
+#include "attn_tile.h"
+#include "internal.h"
+#include "select_impl.h"
+#include "wave.h"
+
+namespace delta {
+namespace {
+
+constexpr int kWaves = kAttnThreads / 64;
+constexpr int kC = kFusedChunkPages;
+constexpr int kRawBufferFlags = 0x00020000;   // buffer-resource word 3, raw access (gfx950)
+constexpr int kCoherent = 16;                 // device-coherent (sc1) cache policy
+// Bound on the polls of the sequence barrier: never reached while every workgroup of the
+// sequence is resident (which the cooperative launch guarantees); it only keeps a broken
+// invariant from hanging the device.
+constexpr int kSpinLimit = 1 << 20;
+
+__device__ __forceinline__ float2 load_ml(const __amdgpu_buffer_rsrc_t& r, int byte_off) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, kCoherent));
+}
+
+template <int D, int G, int U>
+__global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedArgs a) {
+  using Gm = Geo<D>;
+  constexpr int R = Gm::R;
+  const int c = blockIdx.x;
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int quad = lane >> 4, hcol = lane & 15;
+  const int Hq = a.n_q_heads, Hkv = a.n_kv_heads;
+  const int s_b = min(a.seq_lens[b], a.max_seq_len);
+  const int n_pages = (s_b + 15) >> 4;
+  const int n_active = (n_pages + kC - 1) / kC;   // workgroups of this sequence that run
+  if (c >= n_active) return;                      // uniform over the workgroup
+  const int p0 = c * kC;
+  const int np = min(kC, n_pages - p0);
+
+  __shared__ int s_pages[kC];
+  __shared__ float s_p[kWaves][16 * 8 + 8];
+  __shared__ __attribute__((aligned(16))) float s_logit[kFusedMaxQHeads * kC * 16];
+  __shared__ float s_M[kFusedMaxQHeads], s_L[kFusedMaxQHeads], s_lse[kFusedMaxQHeads];
+  __shared__ int s_last;
+  if (tid < np) s_pages[tid] = a.page_table[(size_t)b * a.max_pages + p0 + tid];
+  float* lp = s_p[wave];
+
+  const size_t part_rows = (size_t)gridDim.y * Hkv * a.n_chunks * G;   // rows of G x D / G x 2
+  const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+      a.part_o, 0, (int)min(part_rows * D * 4, (size_t)0x7fffffff), kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rml = __builtin_amdgcn_make_buffer_rsrc(
+      a.part_ml, 0, (int)min(part_rows * 8, (size_t)0x7fffffff), kRawBufferFlags);
+  lds_barrier();   // page list
+
+  // ---- 1. attention over the chunk -----------------------------------------------------
+  for (int g = wave; g < Hkv; g += kWaves) {   // wave-uniform
+    bf16x8 qb[Gm::NK];
+    load_query<D, G>(qb, a.q, (size_t)b * Hq + g * G, lane);
+    WaveSoftmax<G> st;
+    st.init();
+    const size_t head_off = (size_t)g * 16 * D;
+    float* lg = s_logit + (size_t)g * kC * G * 16;
+    // ring of R tiles as in the split kernel; prefetches past the chunk are one-line dummies
+    auto fetch = [&](Tile<D>& t, int k) {
+      const int kk = min(k, np - 1);
+      const size_t page = (size_t)s_pages[kk] * a.page_stride + head_off;
+      const int nrows = min(16, s_b - 16 * (p0 + kk));
+      t.kmask = (nrows >= 16) ? 0xffffu : ((1u << max(nrows, 0)) - 1u);
+      load_page_tile<D>(t, a.k_cache + page, a.v_cache + page, k < np, lane);
+    };
+    Tile<D> t[R];
+#pragma unroll
+    for (int i = 0; i < R - 1; ++i) fetch(t[i], i);
+    for (int k = 0; k < np; k += R) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        fetch(t[(r + R - 1) % R], k + r + R - 1);
+        if (k + r < np)
+          process_tile<D, G, true>(t[r], qb, a.scale_log2, st, lp, lg + (k + r) * G * 16, lane);
+      }
+    }
+    reduce_outputs<D, G>(st);
+    const int prow = (((b * Hkv + g) * a.n_chunks) + c) * G;   // partial row of head 0
+    if (quad == 0 && hcol < G)
+      __builtin_amdgcn_raw_buffer_store_b64(
+          __builtin_bit_cast(u32x2, make_float2(st.m_run, st.l_run)), rml, (prow + hcol) * 8, 0,
+          kCoherent);
+    if (lane < Gm::LPR) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const int off = ((prow + h) * D + 8 * lane) * 4;
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(u32x4, f32x4{st.o[h][0], st.o[h][1], st.o[h][2], st.o[h][3]}), ro,
+            off, 0, kCoherent);
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(u32x4, f32x4{st.o[h][4], st.o[h][5], st.o[h][6], st.o[h][7]}), ro,
+            off + 16, 0, kCoherent);
+      }
+    }
+  }
+
+  // ---- 2. sequence barrier ---------------------------------------------------------------
+  __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores are complete
+  __syncthreads();
+  if (tid == 0) {
+    __hip_atomic_fetch_add(&a.counters[2 * b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int it = 0; it < kSpinLimit &&
+                     __hip_atomic_load(&a.counters[2 * b], __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT) < n_active;
+         ++it)
+      __builtin_amdgcn_s_sleep(2);
+  }
+  __syncthreads();
+
+  // ---- 3. log-sum-exp of every query head ------------------------------------------------
+  // (max, sum) of the chunk partials, folded kBatch chunks at a time with all of a batch's loads
+  // in flight, in chunk order
+  constexpr int kBatch = 16;
+  if (tid < Hq) {
+    const int g = tid / G, h = tid - (tid / G) * G;
+    const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;   // chunk cc: row0 + cc * G
+    float M = kNegInfF, L = 0.f;
+    for (int c0 = 0; c0 < n_active; c0 += kBatch) {
+      float2 ml[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) ml[i] = load_ml(rml, (row0 + min(c0 + i, n_active - 1) * G) * 8);
+      float bm = kNegInfF;
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (c0 + i < n_active) bm = fmaxf(bm, ml[i].x);
+      const float Mn = fmaxf(M, bm);
+      const float Mu = (Mn == kNegInfF) ? 0.f : Mn;
+      L *= exp2f(M - Mu);
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (c0 + i < n_active) L += (ml[i].x == kNegInfF ? 0.f : exp2f(ml[i].x - Mu)) * ml[i].y;
+      M = Mn;
+    }
+    s_M[tid] = M;
+    s_L[tid] = L;
+    s_lse[tid] = M + log2f(L);
+  }
+  __syncthreads();
+
+  // ---- 4. outputs of heads c, c + n_active, ... (chunk order: deterministic) ------------
+  {
+    constexpr int kQuads = D / 4;                       // threads per head
+    constexpr int kHeadsAtOnce = kAttnThreads / kQuads;
+    const int dc = 4 * (tid % kQuads);
+    for (int j = c + n_active * (tid / kQuads); j < Hq; j += n_active * kHeadsAtOnce) {
+      const int g = j / G, h = j - (j / G) * G;
+      const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;
+      const float Mj = s_M[j];
+      f32x4 O = {0.f, 0.f, 0.f, 0.f};
+      for (int c0 = 0; c0 < n_active; c0 += kBatch) {
+        float m[kBatch];
+        f32x4 ov[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+          const int row = row0 + min(c0 + i, n_active - 1) * G;
+          m[i] = load_ml(rml, row * 8).x;
+          ov[i] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, (row * D + dc) * 4, 0, kCoherent));
+        }
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+          if (c0 + i < n_active) O += (m[i] == kNegInfF ? 0.f : exp2f(m[i] - Mj)) * ov[i];
+      }
+      const float lsum = s_L[j];
+      uint2 packed;
+      packed.x = (uint32_t)f32_to_bf16_rne(O[0] / lsum) | ((uint32_t)f32_to_bf16_rne(O[1] / lsum) << 16);
+      packed.y = (uint32_t)f32_to_bf16_rne(O[2] / lsum) | ((uint32_t)f32_to_bf16_rne(O[3] / lsum) << 16);
+      *reinterpret_cast<uint2*>(a.out + ((size_t)b * Hq + j) * D + dc) = packed;
+    }
+  }
+
+  // ---- 5. scores of this chunk's tokens from the LDS logits -------------------------------
+  {
+    const int k = tid >> 2;           // page of the chunk (kC * 4 == kAttnThreads)
+    const int r0 = 4 * (tid & 3);     // its rows r0 .. r0 + 3
+    const int t0 = (p0 + k) * 16 + r0;
+    float acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = a.agg == 0 ? kNegInfF : 0.f;
+    if (k < np) {
+      for (int g = 0; g < Hkv; ++g) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const f32x4 x = *reinterpret_cast<const f32x4*>(
+              &s_logit[(((size_t)g * kC + k) * G + h) * 16 + r0]);
+          const float l = s_lse[g * G + h];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[i] = a.agg == 0 ? fmaxf(acc[i], x[i] - l) : acc[i] + exp2f(x[i] - l);
+        }
+      }
+    }
+    float sc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      sc[i] = (k < np && t0 + i < s_b) ? (a.agg == 0 ? exp2f(acc[i]) : acc[i]) : 0.f;
+    float* S = a.unit_scores + (size_t)b * a.sel.nu_stride;
+    if (U == 16) {
+      float p = (sc[0] + sc[1]) + (sc[2] + sc[3]);
+      p += lane_xor1(p);
+      p += lane_xor2(p);
+      if ((tid & 3) == 0 && k < np)
+        __hip_atomic_store(S + p0 + k, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (k < np && t0 + i < s_b)
+          __hip_atomic_store(S + t0 + i, sc[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  // ---- 6. the last workgroup of the sequence selects ---------------------------------------
+  __builtin_amdgcn_s_waitcnt(0);   // this thread's score stores are complete
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(&a.counters[2 * b + 1], 1, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT) == n_active - 1;
+  __syncthreads();
+  if (!s_last) return;
+  select_sequence<kFusedKeysPerThread, U>(a.sel, b);
+  if (tid == 0) {
+    __hip_atomic_store(&a.counters[2 * b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[2 * b + 1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+static_assert(kC * 4 == kAttnThreads, "scoring gives every thread four tokens of the chunk");
+
+template <int G, int U>
+const void* kernel_of() {
+  return reinterpret_cast<const void*>(&fused_delta_kernel<128, G, U>);
+}
+
+const void* fused_kernel(int group, int unit_tokens) {
+  if (unit_tokens != 16 && unit_tokens != 1) return nullptr;
+  const bool pages = unit_tokens == 16;
+  switch (group) {
+    case 1: return pages ? kernel_of<1, 16>() : kernel_of<1, 1>();
+    case 2: return pages ? kernel_of<2, 16>() : kernel_of<2, 1>();
+    case 3: return pages ? kernel_of<3, 16>() : kernel_of<3, 1>();
+    case 4: return pages ? kernel_of<4, 16>() : kernel_of<4, 1>();
+    case 5: return pages ? kernel_of<5, 16>() : kernel_of<5, 1>();
+    case 6: return pages ? kernel_of<6, 16>() : kernel_of<6, 1>();
+    case 7: return pages ? kernel_of<7, 16>() : kernel_of<7, 1>();
+    case 8: return pages ? kernel_of<8, 16>() : kernel_of<8, 1>();
+    default: return nullptr;
+  }
+}
+
+}  // namespace
+
+int fused_delta_capacity(int head_dim, int group, int unit_tokens) {
+  const void* k = head_dim == 128 ? fused_kernel(group, unit_tokens) : nullptr;
+  if (!k) return 0;
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kAttnThreads, 0) != hipSuccess) return 0;
+  return per_cu * cus;
+}
+
+hipError_t launch_fused_delta(int head_dim, int group, const FusedArgs& a, int batch,
+                              hipStream_t stream) {
+  const void* k = head_dim == 128 ? fused_kernel(group, a.sel.unit_tokens) : nullptr;
+  if (!k) return hipErrorInvalidValue;
+  FusedArgs args = a;
+  void* params[] = {&args};
+  return hipLaunchCooperativeKernel(k, dim3(a.n_chunks, batch), dim3(kAttnThreads), params, 0,
+                                    stream);
+}
+
+}  // namespace delta

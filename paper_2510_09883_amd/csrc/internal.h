@@ -69,6 +69,36 @@ struct SelectArgs {
 
 hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream);
 
+// Fused Delta layer: attention, scoring and selection in one cooperative launch, with the
+// logits kept in LDS.  One workgroup per (chunk of kFusedChunkPages pages, sequence) covers
+// every KV head of the chunk, so the logits a workgroup needs for scoring are its own.
+constexpr int kFusedChunkPages = 64;
+constexpr int kFusedMaxQHeads = 32;      // LDS holds kFusedMaxQHeads x 64 x 16 fp32 logits
+constexpr int kFusedKeysPerThread = 8;   // selection candidates held per thread (2048 units)
+
+struct FusedArgs {
+  const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
+  const uint16_t* v_cache;
+  const int32_t* page_table; // [B, max_pages]
+  const int32_t* seq_lens;   // [B]
+  const uint16_t* q;         // bf16 [B, Hq, D]
+  uint16_t* out;             // bf16 [B, Hq, D]
+  float* part_o;             // [B, Hkv, n_chunks, G, D]  un-normalised chunk outputs
+  float* part_ml;            // [B, Hkv, n_chunks, G, 2]  chunk (max, sum), log2 domain
+  int32_t* counters;         // [B, 2] arrivals after attention / after scoring; zero between launches
+  float* unit_scores;        // [B, sel.nu_stride] page (or token) scores, written here
+  int64_t page_stride;       // elements per physical page = Hkv * 16 * D
+  int32_t n_q_heads, n_kv_heads, max_pages, n_chunks, max_seq_len, agg;
+  float scale_log2;
+  SelectArgs sel;            // unit scores (written here), selection outputs
+};
+
+// Largest grid (chunks x sequences) the fused kernel can keep resident at once on the current
+// device, or 0 when the shape has no fused kernel.
+int fused_delta_capacity(int head_dim, int group, int unit_tokens);
+hipError_t launch_fused_delta(int head_dim, int group, const FusedArgs& a, int batch,
+                              hipStream_t stream);
+
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace delta
