@@ -213,6 +213,225 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps):
 
 
 # ------------------------------------------------------------------------------------------
+# sweeps over the paper's runtime settings (one JSON line per point, after the headline run's
+# protocol: graph-captured steps, inputs resident, rotating input copies below ~1 GiB)
+# ------------------------------------------------------------------------------------------
+def step_tokens(w, roles, s):
+    """Tokens of K/V one DELTA-stack step reads per sequence at context s (for sizing the
+    rotation; selection reads at most the budget)."""
+    n_dense, seen = 0, False
+    for r in roles:
+        seen = seen or r == configs.ROLE_DELTA
+        n_dense += 1 if (r != configs.ROLE_SPARSE or not seen) else 0
+    return n_dense * s + (len(roles) - n_dense) * min(s, w.budget_tokens)
+
+
+def context_sets(base, s, step_bytes):
+    """Input sets at context s (every sequence holding s tokens) over the caches of `base`:
+    copy k reads logical pages [k*n, (k+1)*n) of each sequence's pages, so that consecutive
+    copies touch disjoint memory; as many copies as bring one round of them past 1 GiB (at
+    most 16, and as many as the cached pages hold)."""
+    w = base.workload
+    n = (s + configs.PAGE - 1) // configs.PAGE
+    want = 1 if step_bytes >= (1 << 30) else math.ceil((1 << 30) / max(step_bytes, 1))
+    n_rot = max(1, min(16, want, base.max_pages_per_seq // n))
+    lens_dev = torch.full((w.batch,), s, dtype=torch.int32, device="cuda")
+    sets = []
+    for k in range(n_rot):
+        pt = torch.zeros_like(base.page_table)
+        pt[:, :n] = base.page_table[:, k * n:(k + 1) * n]
+        sets.append(synth.DecodeInputs(w, base.k_cache, base.v_cache, base.q, pt, lens_dev,
+                                       [s] * w.batch, base.max_pages_per_seq, base.n_phys_pages))
+    return sets
+
+
+def stack_us(D, w, sets, roles, shape, sel, ws, steps, warmup):
+    D.delta_workspace_init(ws)
+    st = Stack(D, w, sets, roles, shape, sel, ws)
+    st.capture()
+    us = time_steps(st, steps, warmup) * 1e3
+    del st
+    return us
+
+
+def launch_us(D, w, sets, role, shape, sel, ws, steps):
+    """Average duration of one launch of the FULL or DELTA entry point on layer 0 of each input
+    set, from a graph of one launch per set replayed `steps` times."""
+    D.delta_workspace_init(ws)
+    K = w.budget_units
+    idx = torch.empty((w.batch, K), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((w.batch,), dtype=torch.int32, device="cuda")
+    phys = torch.empty((w.batch, K), dtype=torch.int32, device="cuda")
+    outs = [torch.empty_like(inp.q[0]) for inp in sets]
+
+    def body():
+        for inp, out in zip(sets, outs):
+            kv = D.make_kv(inp.k_cache[0], inp.v_cache[0], inp.page_table, inp.seq_lens)
+            if role == "full":
+                D.delta_full_attn(shape, kv, inp.q[0], out, ws)
+            else:
+                D.delta_delta_attn_select(shape, kv, inp.q[0], out, sel, idx, cnt, None, ws,
+                                          sel_phys=phys)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        body()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        body()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (steps * len(sets))
+
+
+def trapezoid_rounds(points):
+    """Sum over decoding rounds 1..S of a per-round time sampled at contexts `points`
+    ([(context, us)], ascending, first context 1), by linear interpolation: seconds."""
+    tot = 0.0
+    for (c0, t0), (c1, t1) in zip(points, points[1:]):
+        tot += (t0 + t1) / 2 * (c1 - c0)
+    return (tot + points[0][1]) * 1e-6
+
+
+def emit(rec):
+    print(json.dumps(rec), flush=True)
+
+
+def sweep_rounds(D, w, args):
+    """Per-round attention latency while a batch decodes from 1 token to the workload's length
+    (the analogue of the paper's per-round latency trace, Sec. 5.2): full stack vs DELTA stack
+    at sampled contexts, and the attention time summed over every round."""
+    S = w.max_seq_len
+    base = synth.make_inputs(w, "cuda", poison_tail=False)
+    torch.cuda.synchronize()
+    sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+    ws = D.alloc_workspace(D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                        base.max_pages_per_seq, S), sel)
+    ctx = sorted({1, 256, 512, w.budget_tokens, w.budget_tokens + configs.PAGE,
+                  *range(2048, S + 1, 1024), S})
+    full_pts, delta_pts = [], []
+    kv_tok = 4 * w.n_kv_heads * w.head_dim
+    for s in ctx:
+        shape = D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                             base.max_pages_per_seq, s)
+        sets = context_sets(base, s, w.batch * kv_tok * step_tokens(w, w.roles, s))
+        full = stack_us(D, w, sets, [configs.ROLE_FULL] * len(w.roles), shape, sel, ws,
+                        args.steps, args.warmup)
+        delta = stack_us(D, w, sets, w.roles, shape, sel, ws, args.steps, args.warmup)
+        full_pts.append((s, full))
+        delta_pts.append((s, delta))
+        emit({"mode": "rounds", "workload": w.name, "context": s, "full_us": round(full, 2),
+              "delta_us": round(delta, 2), "selecting": (s + w.unit_tokens - 1) // w.unit_tokens > w.budget_units,
+              "input_copies_rotated": len(sets)})
+    tf, td = trapezoid_rounds(full_pts), trapezoid_rounds(delta_pts)
+    emit({"mode": "rounds-summary", "workload": w.describe(), "rounds": S,
+          "delta_layers": w.delta_layers,
+          "attention_s_all_rounds": {"full": round(tf, 3), "delta": round(td, 3)},
+          "attention_tokens_per_s": {"full": round(w.batch * S / tf, 1),
+                                     "delta": round(w.batch * S / td, 1)},
+          "last_round_us": {"full": round(full_pts[-1][1], 2), "delta": round(delta_pts[-1][1], 2)},
+          "first_round_us": {"full": round(full_pts[0][1], 2), "delta": round(delta_pts[0][1], 2)}})
+
+
+def sweep_deltas(D, w, args):
+    """Step time against the number of Delta-layers (Sec. 5.3): at the longest context (the
+    last decoding round) and averaged over all rounds 1..S; the full stack alongside."""
+    S = w.max_seq_len
+    L = w.n_layers
+    base = synth.make_inputs(w, "cuda", poison_tail=False)
+    torch.cuda.synchronize()
+    sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+    ws = D.alloc_workspace(D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                        base.max_pages_per_seq, S), sel)
+    ctx = sorted({1, *range(2048, S + 1, 2048), S})
+    counts = sorted({1, 2, 3, 4, 6, 8, 12, 16, 20, 24, L - 2} & set(range(1, L - 1)))
+    kv_tok = 4 * w.n_kv_heads * w.head_dim
+    per_ctx = {}
+    for s in ctx:
+        shape = D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                             base.max_pages_per_seq, s)
+        # size the rotation for the sparsest schedule, so that no point is served from cache
+        sets = context_sets(base, s, w.batch * kv_tok * step_tokens(
+            w, configs.roles_for(L, [2]), s))
+        full = stack_us(D, w, sets, [configs.ROLE_FULL] * L, shape, sel, ws, args.steps, args.warmup)
+        per_ctx[s] = {"full": full}
+        for c in counts:
+            per_ctx[s][c] = stack_us(D, w, sets, configs.roles_for(L, configs.spread_delta_layers(L, c)),
+                                     shape, sel, ws, args.steps, args.warmup)
+        log(f"context {s}: full {full:.1f} us, " + ", ".join(f"{c}D {per_ctx[s][c]:.1f}" for c in counts))
+    full_avg = trapezoid_rounds([(s, per_ctx[s]["full"]) for s in ctx]) / S * 1e6
+    for c in counts:
+        avg = trapezoid_rounds([(s, per_ctx[s][c]) for s in ctx]) / S * 1e6
+        emit({"mode": "deltas", "workload": w.name, "n_delta": c,
+              "delta_layers": configs.spread_delta_layers(L, c),
+              "last_round_us": round(per_ctx[S][c], 2), "avg_round_us": round(avg, 2),
+              "full_last_round_us": round(per_ctx[S]["full"], 2),
+              "full_avg_round_us": round(full_avg, 2)})
+
+
+def sweep_kl(D, w, args):
+    """DELTA step time over a grid of page budgets K and recency windows L (pages; L < K), at
+    the workload's context (the runtime counterpart of the paper's (K, L) study, Sec. 5.3)."""
+    import dataclasses
+    S = w.max_seq_len
+    base = synth.make_inputs(w, "cuda", poison_tail=False)
+    torch.cuda.synchronize()
+    Ks = [32, 64, 128, 256, 512]
+    Ls = [1, 2, 4, 8, 16, 32, 64]
+    shape = D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, base.max_pages_per_seq, S)
+    big = D.make_select(configs.PAGE * max(Ks), configs.PAGE, w.unit_tokens, D.DELTA_AGG_MAX)
+    ws = D.alloc_workspace(shape, big)
+    kv_tok = 4 * w.n_kv_heads * w.head_dim
+    sets = context_sets(base, S, w.batch * kv_tok * step_tokens(w, w.roles, S))
+    sel0 = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+    full = stack_us(D, w, sets, [configs.ROLE_FULL] * w.n_layers, shape, sel0, ws, args.steps, args.warmup)
+    for K in Ks:
+        for Lp in (l for l in Ls if l < K):
+            wk = dataclasses.replace(w, budget_tokens=configs.PAGE * K, recent_pages=Lp)
+            sel = D.make_select(wk.budget_tokens, wk.recent_tokens, wk.unit_tokens, D.DELTA_AGG_MAX)
+            us = stack_us(D, wk, sets, wk.roles, shape, sel, ws, args.steps, args.warmup)
+            emit({"mode": "kl", "workload": w.name, "context": S, "K_pages": K, "L_pages": Lp,
+                  "delta_us": round(us, 2), "full_us": round(full, 2),
+                  "speedup": round(full / us, 3)})
+
+
+def sweep_overhead(D, args):
+    """Delta-layer overhead over a full layer against context length, per model shape on one
+    GPU without tensor parallelism (the analogue of the paper's kernel breakdown, App. E):
+    per-launch time of the DELTA entry point (attention + logits, scoring, selection) and of
+    the FULL entry point, over a 1k-token budget."""
+    shapes = [("qwen1.5b", 12, 2, 64), ("qwen7b", 28, 4, 64), ("qwen14b", 40, 8, 32)]
+    ctx = [1024, 2048, 4096, 8192, 16384, 32768]
+    for name, hq, hkv, B in shapes:
+        w = configs.Workload(9, f"{name}-b{B}-layer", 1, hq, hkv, 128, B, max(ctx), 1024,
+                             hh_frac=0.02, hh_factor=4.0, recent_pages=8,
+                             roles=[configs.ROLE_DELTA])
+        base = synth.make_inputs(w, "cuda", poison_tail=False)
+        torch.cuda.synchronize()
+        sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+        ws = D.alloc_workspace(D.make_shape(B, hq, hkv, 128, base.max_pages_per_seq, max(ctx)), sel)
+        for s in ctx:
+            shape = D.make_shape(B, hq, hkv, 128, base.max_pages_per_seq, s)
+            sets = context_sets(base, s, B * s * 4 * hkv * 128)
+            f = launch_us(D, w, sets, "full", shape, sel, ws, args.steps)
+            d = launch_us(D, w, sets, "delta", shape, sel, ws, args.steps)
+            emit({"mode": "overhead", "shape": f"{name} Hq/Hkv/d={hq}/{hkv}/128 B={B}",
+                  "context": s, "full_us": round(f, 2), "delta_us": round(d, 2),
+                  "overhead": round((d - f) / f, 4), "input_copies_rotated": len(sets)})
+        del base, ws
+        torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------------------------------
 def cpu_baseline(w, inp, roles, budget_s):
     """The oracle as it stands, on this host: gather + every layer of the DELTA-stack step for
     whole sequences, until `budget_s` seconds are spent; scaled to microseconds per step."""
@@ -285,7 +504,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     # default: the Llama-8B shape at 32K context, batch 16 -- the bandwidth-bound case the
     # targets are stated for (the B = 1, 8K workload is launch-latency bound)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=None, choices=list(range(1, 9)),
+                    help="workload (default 3; the sweeps default to the paper's model for them)")
+    ap.add_argument("--delta-layers", type=str, default=None,
+                    help="comma-separated Delta-layer indices replacing the workload's schedule")
+    ap.add_argument("--sweep", choices=["rounds", "deltas", "kl", "overhead"], default=None,
+                    help="print one JSON line per point of a runtime sweep instead of the "
+                         "headline measurement")
     ap.add_argument("--unit-tokens", type=int, default=16, choices=[16, 1])
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -296,7 +521,20 @@ def main():
         sys.exit(2)
     from paper_2510_09883_amd import delta as D
 
-    w = configs.get(args.config, args.unit_tokens)
+    if args.sweep is not None:
+        default = {"rounds": 6, "deltas": 6, "kl": 7, "overhead": None}[args.sweep]
+        w = configs.get(args.config or default, args.unit_tokens) if default else None
+        if w is not None and args.delta_layers:
+            w.set_delta_layers(args.delta_layers.split(","))
+        if w is not None:
+            log(f"sweep {args.sweep}: {w.describe()}")
+        {"rounds": lambda: sweep_rounds(D, w, args), "deltas": lambda: sweep_deltas(D, w, args),
+         "kl": lambda: sweep_kl(D, w, args), "overhead": lambda: sweep_overhead(D, args)}[args.sweep]()
+        return
+
+    w = configs.get(args.config or 3, args.unit_tokens)
+    if args.delta_layers:
+        w.set_delta_layers(args.delta_layers.split(","))
     lens = synth.seq_lens_for(w)
     fb = full_layer_bytes(w, lens)
     n_delta = sum(r == configs.ROLE_DELTA for r in w.roles)

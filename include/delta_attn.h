@@ -35,7 +35,9 @@
  *             delta_delta_attn_select, the two agree up to floating-point summation order).
  *   Workspace. `ws` is caller-owned device memory of at least delta_workspace_bytes() bytes.
  *             It must be zero-filled once after allocation; every call leaves it ready for the
- *             next call.  Calls that share one workspace must not run concurrently.
+ *             next call with the same shape and selection parameters.  Calls with another
+ *             shape or selection may use it after delta_workspace_init (and when it is large
+ *             enough for them).  Calls that share one workspace must not run concurrently.
  */
 #ifndef DELTA_ATTN_H
 #define DELTA_ATTN_H

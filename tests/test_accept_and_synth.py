@@ -1,6 +1,7 @@
 """CPU tests of the acceptance rule (with ties and near-ties made on purpose) and of the
 seeded input generator."""
 import numpy as np
+import pytest
 import torch
 
 from oracle import accept as A
@@ -66,6 +67,37 @@ def test_workload_table():
     assert (w.budget_units, w.recent_units) == (2048, 128)
     lens = synth.seq_lens_for(configs.get(5))
     assert len(lens) == 32 and min(lens) >= 16384 and max(lens) <= 32768
+    # the runtime settings: K = 64 pages, L = 8 pages, the paper's Delta-layer sets
+    for cid, n, heads, d_set in ((6, 28, (12, 2), [2, 14, 23]), (7, 28, (14, 2), [2, 14, 22]),
+                                 (8, 48, (10, 2), [2, 6, 42])):
+        w = configs.get(cid)
+        assert (w.budget_units, w.recent_units, w.n_layers, len(w.roles)) == (64, 8, n, n)
+        assert (w.n_q_heads, w.n_kv_heads, w.head_dim) == (*heads, 128)
+        assert w.delta_layers == d_set
+        assert w.roles[:2] == [configs.ROLE_FULL] * 2
+        assert all(r == configs.ROLE_SPARSE for i, r in enumerate(w.roles) if i > 2 and i not in d_set)
+
+
+def test_delta_layer_schedules():
+    r = configs.roles_for(8, [5, 2, 2])
+    F, D_, S = configs.ROLE_FULL, configs.ROLE_DELTA, configs.ROLE_SPARSE
+    assert r == [F, F, D_, S, S, D_, S, S]
+    assert configs.roles_for(32, configs.PAPER_DELTA_LAYERS["ds-llama-8b"]).count(D_) == 3
+    for bad in ([], [-1], [8]):
+        with pytest.raises(ValueError):
+            configs.roles_for(8, bad)
+    # the Delta-layer count sweep: the first at layer 2, evenly spread, up to every layer
+    assert configs.spread_delta_layers(28, 1) == [2]
+    assert configs.spread_delta_layers(28, 2) == [2, 27]
+    assert configs.spread_delta_layers(28, 26) == list(range(2, 28))
+    for c in range(1, 27):
+        d = configs.spread_delta_layers(28, c)
+        assert len(d) == c and d[0] == 2 and d == sorted(set(d)) and d[-1] <= 27
+    with pytest.raises(ValueError):
+        configs.spread_delta_layers(28, 27)
+    w = configs.get(3)
+    w.set_delta_layers(configs.PAPER_DELTA_LAYERS["ds-llama-8b"])
+    assert w.delta_layers == [2, 8, 31]
 
 
 def test_generator_deterministic_and_shaped():
