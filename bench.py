@@ -431,6 +431,66 @@ def sweep_overhead(D, args):
         torch.cuda.empty_cache()
 
 
+def sweep_append(D, w, args):
+    """Decode-step integration (Eq. kv_update): the KV append's per-launch time, and the DELTA
+    step with every layer's append enqueued by a before-attention hook of
+    delta_decode_step_hooked, against the same step without appends (both graph-captured)."""
+    lens = synth.seq_lens_for(w)
+    # the appended token is the last one counted by seq_lens, so the step reads it
+    sets = build_sets(w, 1)
+    inp = sets[0]
+    shape = D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, inp.max_pages_per_seq,
+                         inp.max_seq_len)
+    sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+    ws = D.alloc_workspace(shape, sel)
+    g = torch.Generator(device="cuda").manual_seed(1)
+    k_new = [torch.randn((w.batch, w.n_kv_heads, w.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+             for _ in range(w.n_layers)]
+    v_new = [torch.randn_like(k, dtype=torch.float32).to(torch.bfloat16) for k in k_new]
+
+    def append(i):
+        D.delta_kv_append(shape, inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens,
+                          k_new[i], v_new[i])
+
+    def graph_of(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            fn()
+        return gr
+
+    def timed(gr, steps):
+        for _ in range(3):
+            gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps
+
+    us_append = timed(graph_of(lambda: [append(i) for i in range(w.n_layers)]), args.steps) / w.n_layers
+    st = Stack(D, w, sets, w.roles, shape, sel, ws)
+    hooks = D.LayerHooks(before=append)
+    plain = graph_of(lambda: D.delta_decode_step(st.args[0]))
+    hooked = graph_of(lambda: D.delta_decode_step_hooked(st.args[0], hooks))
+    us_plain = timed(plain, args.steps)
+    us_hooked = timed(hooked, args.steps)
+    moved = 4 * w.batch * w.n_kv_heads * w.head_dim * 2   # read k/v_new, write the two rows
+    emit({"mode": "append", "workload": w.describe(), "append_us_per_launch": round(us_append, 2),
+          "append_bytes_per_launch": moved, "delta_step_us": round(us_plain, 2),
+          "delta_step_with_append_hooks_us": round(us_hooked, 2),
+          "append_share_of_step": round((us_hooked - us_plain) / us_plain, 4),
+          "seq_lens_max": max(lens)})
+
+
 # ------------------------------------------------------------------------------------------
 def cpu_baseline(w, inp, roles, budget_s):
     """The oracle as it stands, on this host: gather + every layer of the DELTA-stack step for
@@ -508,7 +568,7 @@ def main():
                     help="workload (default 3; the sweeps default to the paper's model for them)")
     ap.add_argument("--delta-layers", type=str, default=None,
                     help="comma-separated Delta-layer indices replacing the workload's schedule")
-    ap.add_argument("--sweep", choices=["rounds", "deltas", "kl", "overhead"], default=None,
+    ap.add_argument("--sweep", choices=["rounds", "deltas", "kl", "overhead", "append"], default=None,
                     help="print one JSON line per point of a runtime sweep instead of the "
                          "headline measurement")
     ap.add_argument("--unit-tokens", type=int, default=16, choices=[16, 1])
@@ -522,14 +582,15 @@ def main():
     from paper_2510_09883_amd import delta as D
 
     if args.sweep is not None:
-        default = {"rounds": 6, "deltas": 6, "kl": 7, "overhead": None}[args.sweep]
+        default = {"rounds": 6, "deltas": 6, "kl": 7, "overhead": None, "append": 3}[args.sweep]
         w = configs.get(args.config or default, args.unit_tokens) if default else None
         if w is not None and args.delta_layers:
             w.set_delta_layers(args.delta_layers.split(","))
         if w is not None:
             log(f"sweep {args.sweep}: {w.describe()}")
         {"rounds": lambda: sweep_rounds(D, w, args), "deltas": lambda: sweep_deltas(D, w, args),
-         "kl": lambda: sweep_kl(D, w, args), "overhead": lambda: sweep_overhead(D, args)}[args.sweep]()
+         "kl": lambda: sweep_kl(D, w, args), "overhead": lambda: sweep_overhead(D, args),
+         "append": lambda: sweep_append(D, w, args)}[args.sweep]()
         return
 
     w = configs.get(args.config or 3, args.unit_tokens)

@@ -18,8 +18,9 @@
  *             enqueued on `stream` in order.
  *   Errors.   Every call returns a status (DELTA_OK = 0, negative on error).  All argument
  *             checks run on the host before anything is enqueued, so a call that returns an
- *             error has enqueued nothing and left every output untouched.  DELTA_ERR_HIP means
- *             a launch was rejected by the HIP runtime.
+ *             error has enqueued nothing and left every output untouched (except
+ *             DELTA_ERR_HOOK: a caller's hook stopped a hooked step part way).  DELTA_ERR_HIP
+ *             means a launch was rejected by the HIP runtime.
  *   Device-side preconditions (not checked): page-table entries name pages that exist;
  *             1 <= seq_lens[b] <= max_seq_len; inputs are finite; selected indices were made by
  *             delta_delta_attn_select for the same shape and selection parameters.
@@ -54,7 +55,8 @@ enum {
   DELTA_ERR_INVALID_ARG = -1,  /* null pointer, inconsistent sizes, L >= K, ...            */
   DELTA_ERR_UNSUPPORTED = -2,  /* valid but not built: head_dim, group size, page size      */
   DELTA_ERR_WORKSPACE = -3,    /* ws_bytes smaller than delta_workspace_bytes()             */
-  DELTA_ERR_HIP = -4           /* the HIP runtime rejected a launch                          */
+  DELTA_ERR_HIP = -4,          /* the HIP runtime rejected a launch                          */
+  DELTA_ERR_HOOK = -5          /* a delta_decode_step_hooked callback returned non-zero      */
 };
 
 enum { DELTA_ROLE_FULL = 0, DELTA_ROLE_DELTA = 1, DELTA_ROLE_SPARSE = 2 };
@@ -160,6 +162,46 @@ int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_
                       const delta_kv_t* kv, const void* const* q, void* const* out,
                       const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
                       void* ws, size_t ws_bytes, void* stream);
+
+/* KV append (Sec. 2, Eq. kv_update: the cache grows by the decoding token before attention
+ * reads it).  For every sequence b, writes the new token's key and value rows of every KV head
+ * into the paged cache of one layer.  seq_lens[b] already counts the new token, so its row is
+ * s_b - 1: row (s_b - 1) % page_size of physical page page_table[b, (s_b - 1) / page_size].
+ *   k_cache, v_cache: bf16 [n_phys_pages, n_kv_heads, page_size, head_dim], written in place
+ *                     (only those rows);
+ *   page_table, seq_lens: as in delta_kv_t (the caller has already mapped the page);
+ *   k_new, v_new:     bf16 [batch, n_kv_heads, head_dim].
+ * Uses batch, n_kv_heads, head_dim, page_size and max_pages_per_seq of `shape`.  A sequence
+ * with seq_lens[b] < 1 or > max_pages_per_seq * page_size is skipped (nothing is written).
+ * One kernel launch; no workspace; the rows are bitwise copies. */
+int delta_kv_append(const delta_shape_t* shape, void* k_cache, void* v_cache,
+                    const int32_t* page_table, const int32_t* seq_lens, const void* k_new,
+                    const void* v_new, void* stream);
+
+/* Host callbacks around each layer's attention in delta_decode_step_hooked.  A hook runs on
+ * the calling thread while the step is being enqueued, receives the layer index, `user` and
+ * the step's stream, and enqueues its own work on that stream (for example the layer's QKV
+ * projection and delta_kv_append before the attention, the output projection and the FFN
+ * after it), so that its work and the attention launches are ordered and a whole model step
+ * can be captured into one HIP graph.  Return 0 to continue; any other value stops the step. */
+typedef int (*delta_layer_hook_t)(int32_t layer, void* user, void* stream);
+typedef struct {
+  delta_layer_hook_t before_attn;   /* NULL: none */
+  delta_layer_hook_t after_attn;    /* NULL: none */
+  void* user;
+} delta_hooks_t;
+
+/* delta_decode_step with per-layer hooks (App. A, Alg. 1, with the rest of the decoder layer
+ * around each attention: Sec. 2, Eq. gqa_projection, kv_update, gqa_output).  For layer
+ * i = 0 .. n_layers-1: hooks->before_attn(i), the layer's attention as in delta_decode_step,
+ * hooks->after_attn(i).  All arguments are checked before the first hook runs or anything is
+ * enqueued; q[i] and kv[i] may point at buffers that before_attn(i) fills.  When a hook
+ * returns non-zero the step stops and returns DELTA_ERR_HOOK, with the earlier layers' work
+ * already enqueued.  hooks == NULL is delta_decode_step. */
+int delta_decode_step_hooked(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                             const delta_kv_t* kv, const void* const* q, void* const* out,
+                             const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
+                             void* ws, size_t ws_bytes, void* stream, const delta_hooks_t* hooks);
 
 /* Static description of a status code. */
 const char* delta_status_string(int status);

@@ -63,6 +63,22 @@ def gather_tokens(cache_bits: np.ndarray, page_table_row: np.ndarray, seq_len: i
     return out
 
 
+def append_token(cache_bits: np.ndarray, page_table_row: np.ndarray, seq_len: int,
+                 new_bits: np.ndarray, page_size: int = 16) -> np.ndarray:
+    """The KV update of one decoding step for one sequence (Sec. 2, Eq. kv_update): the cache
+    grows by the new token's row, so that attention at this step sees s = seq_len tokens, the
+    last one being the new token.  In the paged layout (Sec. 4 "Page-based DELTA") token
+    s - 1 is row (s - 1) mod P of physical page page_table_row[(s - 1) // P].
+
+    cache_bits: bf16 bits [n_phys_pages, g, P, d]; new_bits: bf16 bits [g, d].  Returns a
+    new array equal to cache_bits except for that row of every KV head.
+    """
+    t = seq_len - 1
+    out = np.array(cache_bits, copy=True)
+    out[int(page_table_row[t // page_size]), :, t % page_size, :] = new_bits
+    return out
+
+
 # --------------------------------------------------------------------------------------------
 # Attention (Sec. 2, Eq. gqa_attention)
 # --------------------------------------------------------------------------------------------

@@ -15,8 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdelta_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["attn_kernel.hip", "fused_delta_kernel.hip", "select_kernel.hip", "probe_kernel.hip",
-           "delta_api.cpp"]
+SOURCES = ["attn_kernel.hip", "fused_delta_kernel.hip", "select_kernel.hip", "append_kernel.hip",
+           "probe_kernel.hip", "delta_api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-mcode-object-version=5",
     # no packed fp32 VALU instructions: scalar/float2 code is compiled to unpacked ops

@@ -383,10 +383,40 @@ int delta_sparse_attn(const delta_shape_t* shape, const delta_kv_t* kv, const vo
                     static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
 
+int delta_kv_append(const delta_shape_t* shape, void* k_cache, void* v_cache,
+                    const int32_t* page_table, const int32_t* seq_lens, const void* k_new,
+                    const void* v_new, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!k_cache || !v_cache || !page_table || !seq_lens || !k_new || !v_new)
+    return DELTA_ERR_INVALID_ARG;
+  AppendArgs a{};
+  a.k_cache = static_cast<uint16_t*>(k_cache);
+  a.v_cache = static_cast<uint16_t*>(v_cache);
+  a.page_table = page_table;
+  a.seq_lens = seq_lens;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.page_stride = (int64_t)shape->n_kv_heads * 16 * shape->head_dim;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.head_dim = shape->head_dim;
+  a.max_pages = shape->max_pages_per_seq;
+  return launch_kv_append(a, shape->batch, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? DELTA_OK : DELTA_ERR_HIP;
+}
+
 int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
                       const delta_kv_t* kv, const void* const* q, void* const* out,
                       const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, void* ws,
                       size_t ws_bytes, void* stream) {
+  return delta_decode_step_hooked(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, ws,
+                                  ws_bytes, stream, nullptr);
+}
+
+int delta_decode_step_hooked(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                             const delta_kv_t* kv, const void* const* q, void* const* out,
+                             const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
+                             void* ws, size_t ws_bytes, void* stream, const delta_hooks_t* hooks) {
   if (n_layers < 0 || (n_layers > 0 && (!roles || !kv || !q || !out)) || !ws)
     return DELTA_ERR_INVALID_ARG;
   int n_delta = 0, n_sel_users = 0;
@@ -415,6 +445,8 @@ int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_
   int32_t* phys = sel ? reinterpret_cast<int32_t*>(w + L.phys) : nullptr;
   const int32_t* phys_pt = nullptr;
   for (int i = 0; i < n_layers; ++i) {
+    if (hooks && hooks->before_attn && hooks->before_attn(i, hooks->user, stream))
+      return DELTA_ERR_HOOK;
     if (roles[i] == DELTA_ROLE_FULL || (roles[i] == DELTA_ROLE_SPARSE && cur < 0)) {
       rc = run_full(shape, &kv[i], q[i], out[i], L, w, st);
     } else if (roles[i] == DELTA_ROLE_DELTA) {
@@ -428,6 +460,8 @@ int delta_decode_step(const delta_shape_t* shape, int32_t n_layers, const int32_
                       kv[i].page_table == phys_pt ? phys : nullptr, L, w, st);
     }
     if (rc) return rc;
+    if (hooks && hooks->after_attn && hooks->after_attn(i, hooks->user, stream))
+      return DELTA_ERR_HOOK;
   }
   return DELTA_OK;
 }
@@ -439,6 +473,7 @@ const char* delta_status_string(int status) {
     case DELTA_ERR_UNSUPPORTED: return "unsupported shape or parameter";
     case DELTA_ERR_WORKSPACE: return "workspace too small";
     case DELTA_ERR_HIP: return "HIP launch failed";
+    case DELTA_ERR_HOOK: return "a layer hook stopped the step";
     default: return "unknown status";
   }
 }

@@ -99,6 +99,20 @@ int fused_delta_capacity(int head_dim, int group, int unit_tokens);
 hipError_t launch_fused_delta(int head_dim, int group, const FusedArgs& a, int batch,
                               hipStream_t stream);
 
+// KV append (Eq. kv_update): the current token's K and V rows into the paged cache.
+struct AppendArgs {
+  uint16_t* k_cache;         // bf16 [pages, Hkv, 16, D]
+  uint16_t* v_cache;
+  const int32_t* page_table; // [B, max_pages]
+  const int32_t* seq_lens;   // [B], counting the new token
+  const uint16_t* k_new;     // bf16 [B, Hkv, D]
+  const uint16_t* v_new;
+  int64_t page_stride;       // elements per physical page = Hkv * 16 * D
+  int32_t n_kv_heads, head_dim, max_pages;
+};
+
+hipError_t launch_kv_append(const AppendArgs& a, int batch, hipStream_t stream);
+
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace delta

@@ -19,12 +19,13 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 DELTA_OK, DELTA_ERR_INVALID_ARG, DELTA_ERR_UNSUPPORTED, DELTA_ERR_WORKSPACE, DELTA_ERR_HIP = 0, -1, -2, -3, -4
+DELTA_ERR_HOOK = -5
 DELTA_ROLE_FULL, DELTA_ROLE_DELTA, DELTA_ROLE_SPARSE = 0, 1, 2
 DELTA_AGG_MAX, DELTA_AGG_SUM = 0, 1
 
 EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
             "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
-            "delta_status_string"]
+            "delta_kv_append", "delta_decode_step_hooked", "delta_status_string"]
 
 
 class delta_shape_t(ctypes.Structure):
@@ -47,6 +48,14 @@ class delta_select_t(ctypes.Structure):
 _P = ctypes.POINTER
 _vp = ctypes.c_void_p
 
+# int (*)(int32_t layer, void* user, void* stream)
+delta_layer_hook_t = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class delta_hooks_t(ctypes.Structure):
+    _fields_ = [("before_attn", delta_layer_hook_t), ("after_attn", delta_layer_hook_t),
+                ("user", ctypes.c_void_p)]
+
 
 def _bind(lib):
     """Declare the C signatures of include/delta_attn.h on a loaded library handle."""
@@ -61,6 +70,10 @@ def _bind(lib):
     lib.delta_decode_step.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
                                       _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
                                       _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.delta_kv_append.argtypes = [_P(delta_shape_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.delta_decode_step_hooked.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
+                                             _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
+                                             _vp, _vp, _vp, ctypes.c_size_t, _vp, _P(delta_hooks_t)]
     lib.delta_hbm_read_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, ctypes.c_int32, _vp]
     lib.delta_hbm_read_probe.restype = ctypes.c_int
     lib.delta_status_string.argtypes = [ctypes.c_int]
@@ -175,6 +188,49 @@ def delta_decode_step(args: StepArgs):
                                   ctypes.byref(a.sel) if a.sel is not None else None,
                                   _ptr(a.sel_idx), _ptr(a.sel_cnt), _ptr(a.ws), _nbytes(a.ws),
                                   _stream()))
+
+
+def delta_kv_append(shape, k_cache, v_cache, page_table, seq_lens, k_new, v_new):
+    _check("delta_kv_append",
+           _lib.delta_kv_append(ctypes.byref(shape), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+                                _ptr(seq_lens), _ptr(k_new), _ptr(v_new), _stream()))
+
+
+class LayerHooks:
+    """Python callables before(layer) / after(layer), run around each layer's attention by
+    delta_decode_step_hooked on the calling thread; they enqueue work on torch's current stream
+    (the step's stream).  An exception in a hook stops the step and is re-raised."""
+
+    def __init__(self, before=None, after=None):
+        self.error = None
+
+        def wrap(fn):
+            if fn is None:
+                return delta_layer_hook_t()
+
+            def cb(layer, user, stream):
+                try:
+                    fn(int(layer))
+                    return 0
+                except BaseException as e:   # noqa: BLE001 - handed back to the caller
+                    self.error = e
+                    return 1
+            return delta_layer_hook_t(cb)
+
+        self._cbs = (wrap(before), wrap(after))
+        self.c = delta_hooks_t(self._cbs[0], self._cbs[1], None)
+
+
+def delta_decode_step_hooked(args: StepArgs, hooks: LayerHooks):
+    a = args
+    hooks.error = None
+    status = _lib.delta_decode_step_hooked(ctypes.byref(a.shape), a.n, a.roles, a.kvs, a.qs, a.outs,
+                                           ctypes.byref(a.sel) if a.sel is not None else None,
+                                           _ptr(a.sel_idx), _ptr(a.sel_cnt), _ptr(a.ws), _nbytes(a.ws),
+                                           _stream(), ctypes.byref(hooks.c))
+    if hooks.error is not None:
+        raise hooks.error
+    _check("delta_decode_step_hooked", status)
 
 
 def delta_hbm_read_probe(buf, sink, n_workgroups=2048, unroll=4):

@@ -24,7 +24,7 @@ def declared_functions(path=HEADER):
 
 def test_library_exports_every_declared_symbol(D):
     names = declared_functions()
-    assert len(names) == 7
+    assert len(names) == 9
     lib = ctypes.CDLL(D.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -135,3 +135,33 @@ def test_calls_reject_before_launch(D):
     assert lib.delta_decode_step(P(s), 3, roles_bad, kvs, ptrs, ptrs, P(sel), fake, fake, fake, need, None) == -1
     nullq = (ctypes.c_void_p * 3)(0x1000, None, 0x1000)
     assert lib.delta_decode_step(P(s), 3, roles, kvs, nullq, ptrs, P(sel), fake, fake, fake, need, None) == -1
+
+
+def test_append_and_hooked_step_reject_before_launch(D):
+    """delta_kv_append and delta_decode_step_hooked check every argument on the host; a
+    rejected hooked step has run no hook."""
+    s = shape(D)
+    sel = D.make_select(2048, 128)
+    lib = D._lib
+    P = ctypes.byref
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.delta_kv_append(P(s), fake, fake, fake, fake, None, fake, None) == -1
+    assert lib.delta_kv_append(P(s), None, fake, fake, fake, fake, fake, None) == -1
+    assert lib.delta_kv_append(P(D.make_shape(2, 32, 8, 80, 512, 8192)), fake, fake, fake, fake,
+                               fake, fake, None) == -2
+    assert lib.delta_kv_append(None, fake, fake, fake, fake, fake, fake, None) == -1
+    calls = []
+    hooks = D.LayerHooks(before=lambda i: calls.append(("before", i)),
+                         after=lambda i: calls.append(("after", i)))
+    kv = D.delta_kv_t(1, 2, 3, 4)
+    roles = (ctypes.c_int32 * 3)(0, 3, 2)          # invalid role
+    kvs = (D.delta_kv_t * 3)(kv, kv, kv)
+    ptrs = (ctypes.c_void_p * 3)(0x1000, 0x1000, 0x1000)
+    need = D.delta_workspace_bytes(s, sel)
+    assert lib.delta_decode_step_hooked(P(s), 3, roles, kvs, ptrs, ptrs, P(sel), fake, fake, fake,
+                                        need, None, P(hooks.c)) == -1
+    roles_ok = (ctypes.c_int32 * 3)(0, 1, 2)
+    assert lib.delta_decode_step_hooked(P(s), 3, roles_ok, kvs, ptrs, ptrs, P(sel), fake, fake, fake,
+                                        16, None, P(hooks.c)) == -3
+    assert calls == []
+    assert D.delta_status_string(-5) == "a layer hook stopped the step"

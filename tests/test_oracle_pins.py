@@ -73,6 +73,27 @@ def test_gather_inverts_independent_scatter(s):
     assert np.array_equal(got, O.bf16_bits_to_f64(tok))
 
 
+@pytest.mark.parametrize("s", [1, 16, 17, 33, 100])
+def test_append_is_concatenation(s):
+    """Eq. kv_update: after the append, the sequence's s tokens are its first s - 1 cached
+    tokens followed by the new token, and no other cache entry changes."""
+    rng = _rng(1000 + s)
+    g, d = 2, 8
+    tok = _bf16_bits(rng.standard_normal((s, g, d)))
+    n_pages = (s + 15) // 16
+    perm = rng.permutation(n_pages + 3)[:n_pages]
+    cache, _ = _paged(tok, perm)
+    new = _bf16_bits(rng.standard_normal((g, d)))
+    got = O.append_token(cache, perm, s, new)
+    full = O.gather_tokens(got, perm, s)
+    assert np.array_equal(full[:s - 1], O.bf16_bits_to_f64(tok[:s - 1]))
+    assert np.array_equal(full[s - 1], O.bf16_bits_to_f64(new))
+    changed = np.argwhere(np.any(got != cache, axis=-1))
+    t = s - 1
+    assert all(tuple(c) in {(perm[t // 16], h, t % 16) for h in range(g)} for c in changed)
+    assert got is not cache
+
+
 # ------------------------------------------------------------------------------------------
 # O3-O5: attention
 # ------------------------------------------------------------------------------------------
