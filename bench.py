@@ -86,12 +86,13 @@ class Stack:
         self.sel_cnt = torch.zeros((n_delta, w.batch), dtype=torch.int32, device="cuda")
         self.sel_phys = torch.zeros((n_delta, w.batch, w.budget_units), dtype=torch.int32, device="cuda")
         self.outs, self.args = [], []
+        n = len(roles)
         for inp in sets:
-            outs = [torch.empty_like(q) for q in inp.q]
+            outs = [torch.empty_like(q) for q in inp.q[:n]]
             kvs = [D.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
-                   for i in range(len(roles))]
+                   for i in range(n)]
             self.outs.append(outs)
-            self.args.append(D.StepArgs(shape, roles, kvs, inp.q, outs, sel, self.sel_idx,
+            self.args.append(D.StepArgs(shape, roles, kvs, inp.q[:n], outs, sel, self.sel_idx,
                                         self.sel_cnt, ws))
         self.graphs = []
 
@@ -526,13 +527,23 @@ def cpu_baseline(w, inp, roles, budget_s):
             "sample": sample, "host_cpus": len(os.sched_getaffinity(0))}
 
 
+ATTN_SOURCES = ("attn_kernel.hip", "attn_tile.h", "wave.h", "internal.h")
+
+
+def attn_source_sha256():
+    """sha256 over the attention kernel's source files, in ATTN_SOURCES order."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2510_09883_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(role, w, kernel_tag):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
     (FETCH_SIZE + WRITE_SIZE, scaled by a known-size copy), or None when there is none for this
     kernel and workload or the kernel source has changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"attn_{role}_{w.name}.md")
-    src = os.path.join(ROOT, "paper_2510_09883_amd", "csrc", "attn_kernel.hip")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -542,7 +553,7 @@ def measured_traffic(role, w, kernel_tag):
             kv[k.strip()] = v.strip()
     if kv.get("kernel") != kernel_tag:
         return None
-    if kv.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    if kv.get("source_sha256") != attn_source_sha256():
         return None
     return int(kv["traffic_bytes_per_launch"])
 
