@@ -129,9 +129,12 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  *                NULL keeps them in the workspace.
  * Launches: the attention kernel (which stages the logits through the workspace), a scoring
  * kernel and a selection kernel.  With DELTA_DELTA_PATH=fused in the environment, shapes with
- * head_dim 128, a multiple of 4 KV heads, at most 32 query heads and at most 2048 candidate
- * units instead run one cooperative kernel that keeps the logits on chip (opt-in: on MI355X its
- * cooperative launch costs more than the logit traffic it saves). */
+ * head_dim 128, a multiple of 4 KV heads, at most 32 query heads, at most 2048 candidate units
+ * and a grid the device holds at once instead run one kernel that keeps the logits on chip
+ * (opt-in: measured on MI355X it is no faster than the split launches).  Its workgroups wait
+ * for the rest of their sequence for at most DELTA_FUSED_SPIN_TICKS ticks of the 100 MHz clock
+ * (default 10 ms) and then hand their part to the sequence's last workgroup, so it never
+ * hangs when not all of them are resident, and gives the same results either way. */
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
                             int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,

@@ -88,7 +88,7 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
 
 struct Layout {
   size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, phys = 0;
-  size_t fcnt = 0;
+  size_t fcnt = 0, fflag = 0;
   size_t total = 0;
   int fused_chunks = 0;   // chunks per sequence of the fused Delta kernel
   int max_split = 0;
@@ -166,7 +166,8 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
     L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
     L->phys = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * (sel->budget_tokens / sel->unit_tokens));
-    L->fcnt = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * 2);
+    L->fcnt = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * 3);
+    L->fflag = off;   off = align_up(off + sizeof(int32_t) * (size_t)s->batch * L->fused_chunks);
   }
   L->total = off;
   return DELTA_OK;
@@ -218,14 +219,12 @@ int run_full(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* 
 
 // `phys` (nullable): where the select kernel also writes the physical location of every
 // selected unit, read through this layer's page table.
-// Whether a Delta layer runs as one fused cooperative launch (logits kept in LDS) instead of
-// attention + scoring + selection launches.  The fused kernel needs head_dim 128, a multiple of
-// 4 KV heads, at most kFusedMaxQHeads query heads, at most 2048 selection candidates, and a grid
-// of (chunks x sequences) that the device keeps resident at once.  It is used only when
-// DELTA_DELTA_PATH=fused is set in the environment: measured on MI355X (Qwen-7B shape, 8 x 32K)
-// a cooperative launch costs about 17 us more than a plain one, and the fused layer took 124 us
-// against 114 us for the split path (107 us with a plain launch, which cannot guarantee the
-// co-residency its sequence barrier needs).
+// Whether a Delta layer runs as one fused launch (logits kept in LDS) instead of attention +
+// scoring + selection launches.  The fused kernel needs head_dim 128, a multiple of 4 KV
+// heads, at most kFusedMaxQHeads query heads, at most 2048 selection candidates, and its grid
+// of (chunks x sequences) must fit on the device at once (otherwise its sequence barrier would
+// mostly run into its time limit and fall back to the slow path).  DELTA_DELTA_PATH=split or
+// =fused in the environment forces either path where the fused kernel applies.
 bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const Layout& L) {
   const char* e = getenv("DELTA_DELTA_PATH");
   if (!e || strcmp(e, "fused")) return false;
@@ -248,6 +247,15 @@ bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const La
   }
   const int cap = cache[dev][G][ui];
   return grid <= cap;
+}
+
+// Longest wait of a fused-kernel workgroup at its sequence barrier: 10 ms of the 100 MHz
+// real-time clock (a resident sequence's workgroups arrive within tens of microseconds of each
+// other).  DELTA_FUSED_SPIN_TICKS overrides it (0: no wait, which forces the fallback of every
+// workgroup but the last to arrive; for tests).
+int64_t fused_spin_ticks() {
+  const char* e = getenv("DELTA_FUSED_SPIN_TICKS");
+  return e ? std::max<int64_t>(0, atoll(e)) : (int64_t)1000000;
 }
 
 int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
@@ -276,6 +284,10 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
     f.part_o = reinterpret_cast<float*>(ws + L.part_o);
     f.part_ml = reinterpret_cast<float*>(ws + L.part_ml);
     f.counters = reinterpret_cast<int32_t*>(ws + L.fcnt);
+    f.chunk_flags = reinterpret_cast<int32_t*>(ws + L.fflag);
+    f.logits = reinterpret_cast<float*>(ws + L.logits);
+    f.logit_pages = L.logit_pages;
+    f.spin_ticks = fused_spin_ticks();
     f.unit_scores = const_cast<float*>(xa.unit_scores);
     f.page_stride = (int64_t)s->n_kv_heads * 16 * s->head_dim;
     f.n_q_heads = s->n_q_heads;

@@ -1,21 +1,27 @@
 // Fused Delta layer for gfx950: full attention, token/page scoring and page selection of one
 // Delta layer (App. A, Alg. 1 Delta branch and Alg. 2 RefreshPages; Sec. 4 "Selection
-// mechanism", "Page-based DELTA") in one cooperative launch, with the logits kept in LDS.
+// mechanism", "Page-based DELTA") in one launch, with the logits kept in LDS.
 //
 // One workgroup per (chunk of kFusedChunkPages pages, sequence) covers every KV head of the
 // chunk: wave w takes KV heads w, w + 4, ... and walks the chunk's pages with the register
 // tile ring of the split attention kernel, putting every scaled log2-domain logit into LDS
 // ([kv head][page][head in group][16]).  Then:
 //   1. each wave stores its chunk partial (max, sum, o) per query head (device-coherent);
-//   2. the workgroups of a sequence wait for each other (device-scope counter; the cooperative
-//      launch guarantees that all of them are resident);
+//   2. the workgroups of a sequence wait for each other (device-scope counter), for at most
+//      a.spin_ticks of the 100 MHz real-time clock;
 //   3. every workgroup forms the log-sum-exp of all query heads from the chunk partials;
 //   4. workgroup c merges the outputs of heads c, c + n_chunks, ... in chunk order;
 //   5. every workgroup scores its own tokens from its LDS logits, s_t = 2^(max_j (x_j(t) -
 //      lse_j)) (or sum_j 2^(x_j(t) - lse_j)), sums them per page and stores the page scores;
 //   6. the last workgroup of the sequence to finish scoring selects for it (select_impl.h).
-// The logits never reach HBM; the split path (attention kernel + score kernel + select
-// kernel) writes and re-reads them.
+// A plain launch does not guarantee that all workgroups of a sequence are resident together.
+// When they are not (the wait of step 2 runs out), the waiting workgroup skips steps 3-5,
+// writes its LDS logits to the workspace and flags its chunk; the sequence's last workgroup
+// then does steps 3-5 for every flagged chunk from the workspace before selecting.  The
+// arithmetic and its order are the same on both paths, so the results are the same bits; no
+// workgroup ever waits without a bound.  When every workgroup is resident the logits never
+// reach HBM; the split path (attention kernel + score kernel + select kernel) writes and
+// re-reads them.
 #include "attn_tile.h"
 #include "internal.h"
 #include "select_impl.h"
@@ -28,9 +34,8 @@ constexpr int kWaves = kAttnThreads / 64;
 constexpr int kC = kFusedChunkPages;
 constexpr int kRawBufferFlags = 0x00020000;   // buffer-resource word 3, raw access (gfx950)
 constexpr int kCoherent = 16;                 // device-coherent (sc1) cache policy
-// Bound on the polls of the sequence barrier: never reached while every workgroup of the
-// sequence is resident (which the cooperative launch guarantees); it only keeps a broken
-// invariant from hanging the device.
+// Bound on the polls of the sequence barrier besides its time limit (each poll is a device
+// round trip plus a short sleep, so this is about a second).
 constexpr int kSpinLimit = 1 << 20;
 
 __device__ __forceinline__ float2 load_ml(const __amdgpu_buffer_rsrc_t& r, int byte_off) {
@@ -117,55 +122,70 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
     }
   }
 
-  // ---- 2. sequence barrier ---------------------------------------------------------------
+  // ---- 2. sequence barrier, bounded in time ----------------------------------------------
+  // A workgroup that does not see every chunk of its sequence arrive within a.spin_ticks (the
+  // other workgroups are not resident: the launch shares the device, or it is larger than what
+  // the device holds at once) does not wait longer: it writes its logits to the workspace and
+  // leaves its chunk to the last workgroup of the sequence (step 6).  Either way the results
+  // are the same bits.
   __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores are complete
   __syncthreads();
+  __shared__ int s_ok;
   if (tid == 0) {
-    __hip_atomic_fetch_add(&a.counters[2 * b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (int it = 0; it < kSpinLimit &&
-                     __hip_atomic_load(&a.counters[2 * b], __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT) < n_active;
-         ++it)
+    __hip_atomic_fetch_add(&a.counters[3 * b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    int ok = 0;
+    for (int it = 0; it < kSpinLimit; ++it) {
+      if (__hip_atomic_load(&a.counters[3 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_active) {
+        ok = 1;
+        break;
+      }
+      if ((int64_t)(__builtin_amdgcn_s_memrealtime() - t0) >= a.spin_ticks) break;
       __builtin_amdgcn_s_sleep(2);
+    }
+    s_ok = ok;
   }
   __syncthreads();
+  const bool ok = s_ok != 0;
 
   // ---- 3. log-sum-exp of every query head ------------------------------------------------
   // (max, sum) of the chunk partials, folded kBatch chunks at a time with all of a batch's loads
   // in flight, in chunk order
   constexpr int kBatch = 16;
-  if (tid < Hq) {
-    const int g = tid / G, h = tid - (tid / G) * G;
-    const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;   // chunk cc: row0 + cc * G
-    float M = kNegInfF, L = 0.f;
-    for (int c0 = 0; c0 < n_active; c0 += kBatch) {
-      float2 ml[kBatch];
+  auto compute_lse = [&]() {
+    if (tid < Hq) {
+      const int g = tid / G, h = tid - (tid / G) * G;
+      const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;   // chunk cc: row0 + cc * G
+      float M = kNegInfF, L = 0.f;
+      for (int c0 = 0; c0 < n_active; c0 += kBatch) {
+        float2 ml[kBatch];
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i) ml[i] = load_ml(rml, (row0 + min(c0 + i, n_active - 1) * G) * 8);
-      float bm = kNegInfF;
+        for (int i = 0; i < kBatch; ++i) ml[i] = load_ml(rml, (row0 + min(c0 + i, n_active - 1) * G) * 8);
+        float bm = kNegInfF;
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i)
-        if (c0 + i < n_active) bm = fmaxf(bm, ml[i].x);
-      const float Mn = fmaxf(M, bm);
-      const float Mu = (Mn == kNegInfF) ? 0.f : Mn;
-      L *= exp2f(M - Mu);
+        for (int i = 0; i < kBatch; ++i)
+          if (c0 + i < n_active) bm = fmaxf(bm, ml[i].x);
+        const float Mn = fmaxf(M, bm);
+        const float Mu = (Mn == kNegInfF) ? 0.f : Mn;
+        L *= exp2f(M - Mu);
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i)
-        if (c0 + i < n_active) L += (ml[i].x == kNegInfF ? 0.f : exp2f(ml[i].x - Mu)) * ml[i].y;
-      M = Mn;
+        for (int i = 0; i < kBatch; ++i)
+          if (c0 + i < n_active) L += (ml[i].x == kNegInfF ? 0.f : exp2f(ml[i].x - Mu)) * ml[i].y;
+        M = Mn;
+      }
+      s_M[tid] = M;
+      s_L[tid] = L;
+      s_lse[tid] = M + log2f(L);
     }
-    s_M[tid] = M;
-    s_L[tid] = L;
-    s_lse[tid] = M + log2f(L);
-  }
-  __syncthreads();
+    __syncthreads();
+  };
 
-  // ---- 4. outputs of heads c, c + n_active, ... (chunk order: deterministic) ------------
-  {
+  // ---- 4. outputs of heads cc, cc + n_active, ... (chunk order: deterministic) -----------
+  auto merge_outputs = [&](int cc) {
     constexpr int kQuads = D / 4;                       // threads per head
     constexpr int kHeadsAtOnce = kAttnThreads / kQuads;
     const int dc = 4 * (tid % kQuads);
-    for (int j = c + n_active * (tid / kQuads); j < Hq; j += n_active * kHeadsAtOnce) {
+    for (int j = cc + n_active * (tid / kQuads); j < Hq; j += n_active * kHeadsAtOnce) {
       const int g = j / G, h = j - (j / G) * G;
       const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;
       const float Mj = s_M[j];
@@ -190,22 +210,32 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
       packed.y = (uint32_t)f32_to_bf16_rne(O[2] / lsum) | ((uint32_t)f32_to_bf16_rne(O[3] / lsum) << 16);
       *reinterpret_cast<uint2*>(a.out + ((size_t)b * Hq + j) * D + dc) = packed;
     }
-  }
+  };
 
-  // ---- 5. scores of this chunk's tokens from the LDS logits -------------------------------
-  {
+  // ---- 5. scores of chunk cc's tokens, from this workgroup's LDS logits or from the
+  // workspace copy a timed-out workgroup left (layout [b][kv head][page][head in group][16])
+  auto score_chunk = [&](int cc, bool from_lds) {
+    const int pc = cc * kC;
+    const int npc = min(kC, n_pages - pc);
     const int k = tid >> 2;           // page of the chunk (kC * 4 == kAttnThreads)
     const int r0 = 4 * (tid & 3);     // its rows r0 .. r0 + 3
-    const int t0 = (p0 + k) * 16 + r0;
+    const int t0 = (pc + k) * 16 + r0;
     float acc[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = a.agg == 0 ? kNegInfF : 0.f;
-    if (k < np) {
+    if (k < npc) {
       for (int g = 0; g < Hkv; ++g) {
+        const float* glog = a.logits + (((size_t)b * Hkv + g) * a.logit_pages + pc + k) * G * 16 + r0;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          const f32x4 x = *reinterpret_cast<const f32x4*>(
-              &s_logit[(((size_t)g * kC + k) * G + h) * 16 + r0]);
+          f32x4 x;
+          if (from_lds) {
+            x = *reinterpret_cast<const f32x4*>(&s_logit[(((size_t)g * kC + k) * G + h) * 16 + r0]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              x[i] = __hip_atomic_load(glog + h * 16 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
           const float l = s_lse[g * G + h];
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -216,34 +246,74 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
     float sc[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      sc[i] = (k < np && t0 + i < s_b) ? (a.agg == 0 ? exp2f(acc[i]) : acc[i]) : 0.f;
+      sc[i] = (k < npc && t0 + i < s_b) ? (a.agg == 0 ? exp2f(acc[i]) : acc[i]) : 0.f;
     float* S = a.unit_scores + (size_t)b * a.sel.nu_stride;
     if (U == 16) {
       float p = (sc[0] + sc[1]) + (sc[2] + sc[3]);
       p += lane_xor1(p);
       p += lane_xor2(p);
-      if ((tid & 3) == 0 && k < np)
-        __hip_atomic_store(S + p0 + k, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((tid & 3) == 0 && k < npc)
+        __hip_atomic_store(S + pc + k, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (k < np && t0 + i < s_b)
+        if (k < npc && t0 + i < s_b)
           __hip_atomic_store(S + t0 + i, sc[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  };
+
+  int32_t* deferred = a.chunk_flags + (size_t)b * a.n_chunks;
+  if (ok) {
+    compute_lse();
+    merge_outputs(c);
+    score_chunk(c, true);
+  } else {
+    // leave the chunk to the sequence's last workgroup: its logits go to the workspace
+    for (int g = 0; g < Hkv; ++g) {
+      float* dst = a.logits + (((size_t)b * Hkv + g) * a.logit_pages + p0) * G * 16;
+      const float* src = s_logit + (size_t)g * kC * G * 16;
+      for (int i = tid; i < np * G * 16; i += kAttnThreads)
+        __hip_atomic_store(dst + i, src[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (tid == 0) {
+      __hip_atomic_store(deferred + c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.counters[3 * b + 2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 
-  // ---- 6. the last workgroup of the sequence selects ---------------------------------------
-  __builtin_amdgcn_s_waitcnt(0);   // this thread's score stores are complete
+  // ---- 6. the last workgroup of the sequence finishes left chunks and selects --------------
+  __builtin_amdgcn_s_waitcnt(0);   // this thread's score / logit / flag stores are complete
   __syncthreads();
   if (tid == 0)
-    s_last = __hip_atomic_fetch_add(&a.counters[2 * b + 1], 1, __ATOMIC_RELAXED,
+    s_last = __hip_atomic_fetch_add(&a.counters[3 * b + 1], 1, __ATOMIC_RELAXED,
                                     __HIP_MEMORY_SCOPE_AGENT) == n_active - 1;
   __syncthreads();
   if (!s_last) return;
+  // every workgroup of the sequence has arrived (so every partial is stored) and has either
+  // scored its chunk or left it
+  __shared__ int s_flag;
+  if (tid == 0) s_flag = __hip_atomic_load(&a.counters[3 * b + 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (s_flag) {
+    if (!ok) compute_lse();
+    for (int cc = 0; cc < n_active; ++cc) {
+      if (tid == 0) s_flag = __hip_atomic_load(deferred + cc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      if (s_flag) {
+        merge_outputs(cc);
+        score_chunk(cc, false);
+        if (tid == 0) __hip_atomic_store(deferred + cc, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      __syncthreads();
+    }
+    __builtin_amdgcn_s_waitcnt(0);   // the scores written here are complete before selecting
+    __syncthreads();
+  }
   select_sequence<kFusedKeysPerThread, U>(a.sel, b);
   if (tid == 0) {
-    __hip_atomic_store(&a.counters[2 * b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&a.counters[2 * b + 1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[3 * b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[3 * b + 1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[3 * b + 2], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -286,10 +356,22 @@ hipError_t launch_fused_delta(int head_dim, int group, const FusedArgs& a, int b
                               hipStream_t stream) {
   const void* k = head_dim == 128 ? fused_kernel(group, a.sel.unit_tokens) : nullptr;
   if (!k) return hipErrorInvalidValue;
-  FusedArgs args = a;
-  void* params[] = {&args};
-  return hipLaunchCooperativeKernel(k, dim3(a.n_chunks, batch), dim3(kAttnThreads), params, 0,
-                                    stream);
+  switch (group) {
+#define DELTA_FUSED_CASE(GG)                                                                  \
+  case GG:                                                                                    \
+    if (a.sel.unit_tokens == 16)                                                              \
+      hipLaunchKernelGGL((fused_delta_kernel<128, GG, 16>), dim3(a.n_chunks, batch),          \
+                         dim3(kAttnThreads), 0, stream, a);                                   \
+    else                                                                                      \
+      hipLaunchKernelGGL((fused_delta_kernel<128, GG, 1>), dim3(a.n_chunks, batch),           \
+                         dim3(kAttnThreads), 0, stream, a);                                   \
+    break;
+    DELTA_FUSED_CASE(1) DELTA_FUSED_CASE(2) DELTA_FUSED_CASE(3) DELTA_FUSED_CASE(4)
+    DELTA_FUSED_CASE(5) DELTA_FUSED_CASE(6) DELTA_FUSED_CASE(7) DELTA_FUSED_CASE(8)
+#undef DELTA_FUSED_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace delta

@@ -69,9 +69,9 @@ struct SelectArgs {
 
 hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream);
 
-// Fused Delta layer: attention, scoring and selection in one cooperative launch, with the
-// logits kept in LDS.  One workgroup per (chunk of kFusedChunkPages pages, sequence) covers
-// every KV head of the chunk, so the logits a workgroup needs for scoring are its own.
+// Fused Delta layer: attention, scoring and selection in one launch, with the logits kept in
+// LDS.  One workgroup per (chunk of kFusedChunkPages pages, sequence) covers every KV head of
+// the chunk, so the logits a workgroup needs for scoring are its own.
 constexpr int kFusedChunkPages = 64;
 constexpr int kFusedMaxQHeads = 32;      // LDS holds kFusedMaxQHeads x 64 x 16 fp32 logits
 constexpr int kFusedKeysPerThread = 8;   // selection candidates held per thread (2048 units)
@@ -85,15 +85,19 @@ struct FusedArgs {
   uint16_t* out;             // bf16 [B, Hq, D]
   float* part_o;             // [B, Hkv, n_chunks, G, D]  un-normalised chunk outputs
   float* part_ml;            // [B, Hkv, n_chunks, G, 2]  chunk (max, sum), log2 domain
-  int32_t* counters;         // [B, 2] arrivals after attention / after scoring; zero between launches
+  int32_t* counters;         // [B, 3] arrivals after attention, arrivals after scoring, "a
+                             // chunk was left to the last workgroup"; zero between launches
+  int32_t* chunk_flags;      // [B, n_chunks] chunk left to the last workgroup; zero between launches
+  float* logits;             // [B, Hkv, logit_pages, G, 16] logits of left chunks (workspace)
   float* unit_scores;        // [B, sel.nu_stride] page (or token) scores, written here
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
-  int32_t n_q_heads, n_kv_heads, max_pages, n_chunks, max_seq_len, agg;
+  int64_t spin_ticks;        // longest wait at the sequence barrier, 100 MHz clock ticks
+  int32_t n_q_heads, n_kv_heads, max_pages, n_chunks, max_seq_len, agg, logit_pages;
   float scale_log2;
   SelectArgs sel;            // unit scores (written here), selection outputs
 };
 
-// Largest grid (chunks x sequences) the fused kernel can keep resident at once on the current
+// Largest grid (chunks x sequences) the fused kernel can have resident at once on the current
 // device, or 0 when the shape has no fused kernel.
 int fused_delta_capacity(int head_dim, int group, int unit_tokens);
 hipError_t launch_fused_delta(int head_dim, int group, const FusedArgs& a, int batch,

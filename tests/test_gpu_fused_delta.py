@@ -1,10 +1,11 @@
 """GPU parity of the fused Delta-layer kernel (attention, scoring and selection in one
 cooperative launch, logits kept in LDS) against the CPU oracle.
 
-The fused kernel runs where it fits when DELTA_DELTA_PATH=fused is set (it is not the default:
-its cooperative launch costs more than it saves on MI355X).  Here it runs on short, ragged and
-multi-chunk sequences of the Qwen-7B shape, with both aggregations and both unit sizes, and is
-compared with the oracle and with the split path.
+The fused kernel runs where it fits when DELTA_DELTA_PATH=fused is set.  Here it runs on
+short, ragged and multi-chunk sequences of the Qwen-7B shape, with both aggregations and both
+unit sizes, and is compared with the oracle and with the split path.  Its fallback (a
+workgroup whose sequence barrier times out leaves its chunk to the sequence's last workgroup)
+is forced from the host with a zero wait and must give the same bits.
 """
 import numpy as np
 import pytest
@@ -118,3 +119,29 @@ def test_fused_delta_in_decode_step(monkeypatch):
     res = run_step(inp, roles=roles)
     check_step(inp, res, roles=roles, layers=[0, 1, 2, 3]).assert_ok()
     log("fused Delta step ok")
+
+
+@pytest.mark.parametrize("U", [16, 1])
+def test_fused_barrier_fallback_gives_the_same_bits(monkeypatch, U):
+    """With no wait at the sequence barrier every workgroup but the last to arrive leaves its
+    chunk (logits to the workspace); the last one merges, scores and selects for all of them.
+    Outputs, scores and selections equal the normal fused run bit for bit, and the oracle."""
+    lens = [2100, 1000, 17] if U == 1 else [4000, 1000, 17]
+    inp = _qwen(U, lens)
+    n_u = (max(lens) + U - 1) // U
+    monkeypatch.setenv("DELTA_DELTA_PATH", "fused")
+    sc_a = torch.full((len(lens), n_u), -1.0, device="cuda")
+    out_a, idx_a, cnt_a, phys_a, ws = _delta_call(inp, 0, scores=sc_a)
+    monkeypatch.setenv("DELTA_FUSED_SPIN_TICKS", "0")
+    sc_b = torch.full((len(lens), n_u), -1.0, device="cuda")
+    out_b, idx_b, cnt_b, phys_b, _ = _delta_call(inp, 0, scores=sc_b, ws=ws)
+    _check(inp, 0, out_b, idx_b, cnt_b, phys_b)
+    assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16))
+    assert torch.equal(sc_a, sc_b)
+    assert torch.equal(idx_a, idx_b) and torch.equal(cnt_a, cnt_b) and torch.equal(phys_a, phys_b)
+    # the workspace is re-armed: a normal call after the fallback gives the same bits again
+    monkeypatch.delenv("DELTA_FUSED_SPIN_TICKS")
+    sc_c = torch.full((len(lens), n_u), -1.0, device="cuda")
+    out_c, idx_c, _, _, _ = _delta_call(inp, 0, scores=sc_c, ws=ws)
+    assert torch.equal(out_a.view(torch.int16), out_c.view(torch.int16)) and torch.equal(sc_a, sc_c)
+    assert torch.equal(idx_a, idx_c)
