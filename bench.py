@@ -527,7 +527,7 @@ def cpu_baseline(w, inp, roles, budget_s):
             "sample": sample, "host_cpus": len(os.sched_getaffinity(0))}
 
 
-ATTN_SOURCES = ("attn_kernel.hip", "attn_tile.h", "wave.h", "internal.h")
+ATTN_SOURCES = ("attn_kernel.hip", "attn_tile.h", "wave.h")
 
 
 def attn_source_sha256():
