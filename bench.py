@@ -9,10 +9,13 @@ touches less than ~1 GiB, several copies of the inputs are rotated so that the 2
 Infinity Cache cannot serve a step from the previous one.
 
 Printed JSON line (rank 0, N = 1): value = DELTA-stack microseconds per step (lower is
-better), with the full stack, tokens/s, algorithmic HBM GB/s, per-role layer times, the
-Delta-select overhead, the roofline of the dominant kernel (per-launch time from HIP events
-around graph-captured launches of that role on the launch stream) and the CPU oracle timed on
-this host.
+better), with the full stack, the per-step median / p10 / p90, tokens/s, algorithmic HBM GB/s,
+per-role layer times and their fractions of the 8 TB/s peak and of the read rate a plain
+streaming kernel reaches on this GPU, the Delta-select overhead, the roofline of the dominant
+kernel (per-launch time from HIP events around graph-captured launches of that role on the
+launch stream) and the CPU oracle timed on this host.
+
+With --sweep, one JSON line per point of a runtime sweep over the paper's settings instead.
 """
 from __future__ import annotations
 
@@ -130,6 +133,49 @@ def time_steps(stack, steps, warmup):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / steps   # ms per step
+
+
+def step_distribution(stack, steps):
+    """Per-step times (us) from HIP events between consecutive replays: median, p10, p90."""
+    import numpy as np
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for k in range(steps):
+        stack.replay(k)
+        ev[k + 1].record()
+    torch.cuda.synchronize()
+    t = np.array([ev[k].elapsed_time(ev[k + 1]) * 1e3 for k in range(steps)])
+    return {"median": round(float(np.median(t)), 2), "p10": round(float(np.percentile(t, 10)), 2),
+            "p90": round(float(np.percentile(t, 90)), 2)}
+
+
+def read_ceiling(D):
+    """The best streaming-read rate of the probe kernel (include/delta_probe.h) over a 4 GiB
+    buffer, over a few launch shapes, each timed over 8 launches after 2 untimed ones: the
+    read bandwidth this GPU delivers to a plain streaming kernel, beside the data-sheet peak."""
+    nbytes = 4 << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    best = (0.0, None)
+    for wgs in (256, 512, 1024, 2048):
+        for unroll in (2, 4, 8):
+            sink = torch.zeros(wgs, dtype=torch.int32, device="cuda")
+            for _ in range(2):
+                D.delta_hbm_read_probe(buf, sink, wgs, unroll)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(8):
+                D.delta_hbm_read_probe(buf, sink, wgs, unroll)
+            e1.record()
+            torch.cuda.synchronize()
+            gbps = nbytes * 8 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+            log(f"read probe: {wgs} workgroups, unroll {unroll}: {gbps:.0f} GB/s")
+            if gbps > best[0]:
+                best = (gbps, f"{wgs} workgroups, {unroll} loads in flight per thread")
+    del buf
+    torch.cuda.empty_cache()
+    return {"gbps": round(best[0], 1), "buffer": "4 GiB", "launch": best[1],
+            "kernel": "delta_hbm_read_probe (16-byte streaming loads)"}
 
 
 def time_layers(D, w, sets, stack, shape, sel, ws, steps):
@@ -523,8 +569,16 @@ def cpu_baseline(w, inp, roles, budget_s):
     us_per_step = spent / done * w.batch * 1e6
     sample = (f"oracle DELTA-stack step (gather + {len(roles)} layers) of {done} of {w.batch} "
               f"sequence(s), {spent:.1f} s; per-step value scaled by {w.batch}/{done}")
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:   # pragma: no cover
+        pass
     return {"value": us_per_step, "unit": "us/step", "cores": threads, "kind": "oracle",
-            "sample": sample, "host_cpus": len(os.sched_getaffinity(0))}
+            "sample": sample, "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
 
 
 ATTN_SOURCES = ("attn_kernel.hip", "attn_tile.h", "wave.h")
@@ -630,6 +684,8 @@ def main():
     ms_full = time_steps(full_stack, args.steps, args.warmup)
     ms_delta = time_steps(delta_stack, args.steps, args.warmup)
     log(f"full stack {ms_full * 1e3:.1f} us/step, DELTA stack {ms_delta * 1e3:.1f} us/step")
+    dist = {"delta": step_distribution(delta_stack, args.steps),
+            "full": step_distribution(full_stack, args.steps)}
 
     # algorithmic bytes of one DELTA step from the selections it made
     idx = delta_stack.sel_idx.cpu().numpy()
@@ -662,6 +718,9 @@ def main():
     achieved = role_bytes[dominant] / (layer_us[dominant] * 1e-6) / 1e9
     overhead = (layer_us["delta"] - layer_us["full"]) / layer_us["full"] if "delta" in layer_us and "full" in layer_us else None
 
+    ceiling = read_ceiling(D)
+    log(f"measured read ceiling {ceiling}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -693,6 +752,7 @@ def main():
             "input_copies_rotated": n_sets, "graph": True,
         },
         "full_stack_us_per_step": round(ms_full * 1e3, 2),
+        "step_us_distribution": dist,
         "delta_speedup_vs_full": round(ms_full / ms_delta, 3),
         "tokens_per_s": {"delta": round(w.batch / (ms_delta * 1e-3), 1),
                          "full": round(w.batch / (ms_full * 1e-3), 1)},
@@ -702,6 +762,11 @@ def main():
                          "full_stack": round(full_bytes / (ms_full * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
         "layer_us": {k: round(v, 2) for k, v in layer_us.items()},
         "layer_gbps": {k: round(role_bytes[k] / (layer_us[k] * 1e-6) / 1e9, 1) for k in layer_us},
+        "layer_frac_of_peak": {k: round(role_bytes[k] / (layer_us[k] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+                               for k in layer_us},
+        "measured_read_ceiling": ceiling,
+        "layer_frac_of_measured_ceiling": {k: round(role_bytes[k] / (layer_us[k] * 1e-6) / 1e9 / ceiling["gbps"], 4)
+                                           for k in layer_us},
         "delta_select_overhead": None if overhead is None else round(overhead, 4),
         "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),

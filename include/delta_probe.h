@@ -14,9 +14,9 @@ extern "C" {
 #endif
 
 /* Reads `bytes` bytes (rounded down to 16) of device buffer `buf` (16-byte aligned) with
- * `n_workgroups` workgroups of 256 threads, each thread keeping `unroll` (1, 2, 4 or 8)
- * 16-byte loads in flight, and writes one word per workgroup to device array
- * sink[n_workgroups].  Enqueued on `stream` (hipStream_t as void*); no synchronisation.
+ * `n_workgroups` workgroups of 256 threads, each streaming its own contiguous share with
+ * non-temporal loads, each thread keeping `unroll` (1, 2, 4 or 8) 16-byte loads in flight, and
+ * writes one word per workgroup to device array sink[n_workgroups].  Enqueued on `stream` (hipStream_t as void*); no synchronisation.
  * Returns 0, -1 for a bad argument (nothing enqueued), -4 if the launch failed. */
 int delta_hbm_read_probe(const void* buf, size_t bytes, uint32_t* sink, int32_t n_workgroups,
                          int32_t unroll, void* stream);

@@ -2,8 +2,11 @@
 // bandwidth the memory system actually delivers (the denominator the attention kernels are
 // compared with, next to the 8 TB/s data-sheet peak).
 //
-// Every thread reads 16-byte words in a grid-stride loop, UNROLL loads in flight at a time,
-// and folds them with XOR so the loads cannot be removed; one word per workgroup is written.
+// Every workgroup streams its own contiguous share of the buffer, as the attention kernels'
+// workgroups stream their pages: per step the 256 threads read UNROLL x 4 KB contiguous bytes
+// (16 bytes per thread and load, one 1 KB run per wave and load) with non-temporal loads, all
+// UNROLL loads of a step in flight at once, folded with XOR so the loads cannot be removed;
+// one word per workgroup is written.
 #include "../../include/delta_probe.h"
 
 #include <hip/hip_runtime.h>
@@ -16,24 +19,28 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 template <int UNROLL>
 __global__ __launch_bounds__(256) void read_probe_kernel(const u32x4* __restrict__ src, size_t n,
                                                          uint32_t* __restrict__ sink) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  // this workgroup's words [lo, hi)
+  const size_t per = n / gridDim.x;
+  const size_t lo = (size_t)blockIdx.x * per;
+  const size_t hi = blockIdx.x + 1 == gridDim.x ? n : lo + per;
+  const int t = threadIdx.x;
   u32x4 acc = {0u, 0u, 0u, 0u};
-  for (; i + (UNROLL - 1) * stride < n; i += UNROLL * stride) {
+  size_t i = lo;
+  for (; i + (size_t)UNROLL * 256 <= hi; i += (size_t)UNROLL * 256) {
     u32x4 v[UNROLL];
 #pragma unroll
-    for (int u = 0; u < UNROLL; ++u) v[u] = src[i + u * stride];
+    for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(src + i + u * 256 + t);
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) acc ^= v[u];
   }
-  for (; i < n; i += stride) acc ^= src[i];
+  for (i += t; i < hi; i += 256) acc ^= src[i];
   uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
   __shared__ uint32_t s[256];
-  s[threadIdx.x] = x;
+  s[t] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (t == 0) {
     uint32_t r = 0;
-    for (int t = 0; t < 256; ++t) r ^= s[t];
+    for (int k = 0; k < 256; ++k) r ^= s[k];
     sink[blockIdx.x] = r;
   }
 }
