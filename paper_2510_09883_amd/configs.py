@@ -122,7 +122,7 @@ class Workload:
         return self.seq_len_range[1] if self.seq_len_range else self.seq_len
 
     def describe(self):
-        return (f"cfg{self.cfg_id} {self.name}: {self.n_layers} layers, Hq/Hkv/d="
+        return (f"{self.name}: {self.n_layers} layers, Hq/Hkv/d="
                 f"{self.n_q_heads}/{self.n_kv_heads}/{self.head_dim}, B={self.batch}, "
                 f"s={'U%s' % (self.seq_len_range,) if self.seq_len_range else self.seq_len}, "
                 f"K={self.budget_tokens} tok, L={self.recent_tokens} tok, U={self.unit_tokens}")
