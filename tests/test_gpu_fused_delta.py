@@ -1,5 +1,5 @@
 """GPU parity of the fused Delta-layer kernel (attention, scoring and selection in one
-cooperative launch, logits kept in LDS) against the CPU oracle.
+launch, logits kept in LDS) against the CPU oracle.
 
 The fused kernel runs where it fits when DELTA_DELTA_PATH=fused is set.  Here it runs on
 short, ragged and multi-chunk sequences of the Qwen-7B shape, with both aggregations and both
