@@ -569,6 +569,23 @@ def cpu_baseline(w, inp, roles, budget_s):
     us_per_step = spent / done * w.batch * 1e6
     sample = (f"oracle DELTA-stack step (gather + {len(roles)} layers) of {done} of {w.batch} "
               f"sequence(s), {spent:.1f} s; per-step value scaled by {w.batch}/{done}")
+    # oracle seconds per (sequence, layer) for each role, on sequence 0's first layer
+    host = synth.sequence_pages(inp, 0, 0)
+    s0 = inp.seq_lens_host[0]
+    ident = np.arange(host[0].shape[0])
+    K0, V0 = O.gather_tokens(host[0], ident, s0), O.gather_tokens(host[1], ident, s0)
+    q0 = O.bf16_bits_to_f64(synth.bits(inp.q[0][0]))
+    per_role = {}
+    t = time.perf_counter()
+    _, alpha = O.full_attention(q0, K0, V0, scale)
+    per_role["full"] = time.perf_counter() - t
+    t = time.perf_counter()
+    _, alpha = O.full_attention(q0, K0, V0, scale)
+    rho, _ = O.refresh_units(alpha, w.unit_tokens, w.budget_units, w.recent_units)
+    per_role["delta"] = time.perf_counter() - t
+    t = time.perf_counter()
+    O.sparse_attention(q0, K0, V0, rho, w.unit_tokens, scale)
+    per_role["sparse"] = time.perf_counter() - t
     model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -578,7 +595,8 @@ def cpu_baseline(w, inp, roles, budget_s):
     except OSError:   # pragma: no cover
         pass
     return {"value": us_per_step, "unit": "us/step", "cores": threads, "kind": "oracle",
-            "sample": sample, "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
+            "sample": sample, "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model,
+            "seconds_per_sequence_layer": {k: round(v, 4) for k, v in per_role.items()}}
 
 
 ATTN_SOURCES = ("attn_kernel.hip", "attn_tile.h", "wave.h")

@@ -60,3 +60,13 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_cpu_baseline_reports_cores_and_per_role_times():
+    from paper_2510_09883_amd import synth
+    w = configs.get(1)
+    inp = synth.make_inputs(w, "cpu", poison_tail=False)
+    r = bench.cpu_baseline(w, inp, w.roles, 0.5)
+    assert r["kind"] == "oracle" and r["unit"] == "us/step" and r["value"] > 0
+    assert r["cores"] >= 1 and r["host_cpus"] >= 1
+    assert set(r["seconds_per_sequence_layer"]) == {"full", "delta", "sparse"}
