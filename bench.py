@@ -550,7 +550,7 @@ def cpu_baseline(w, inp, roles, budget_s):
     except Exception:   # pragma: no cover
         threads = 1
     scale = O.default_scale(w.head_dim)
-    done, spent = 0, 0.0
+    done, spent, toks = 0, 0.0, 0
     for b in range(w.batch):
         host = [synth.sequence_pages(inp, i, b) for i in range(len(roles))]
         qs = [O.bf16_bits_to_f64(synth.bits(inp.q[i][b])) for i in range(len(roles))]
@@ -563,12 +563,18 @@ def cpu_baseline(w, inp, roles, budget_s):
                                w.recent_units)
         spent += time.perf_counter() - t
         done += 1
+        toks += s_b
         del host, Ks, Vs
         if spent >= budget_s:
             break
-    us_per_step = spent / done * w.batch * 1e6
+    # the oracle's work grows linearly with a sequence's length: scale by tokens
+    total = sum(inp.seq_lens_host)
+    us_per_step = spent / toks * total * 1e6
     sample = (f"oracle DELTA-stack step (gather + {len(roles)} layers) of {done} of {w.batch} "
-              f"sequence(s), {spent:.1f} s; per-step value scaled by {w.batch}/{done}")
+              f"sequence(s) ({toks} of {total} tokens), {spent:.1f} s; the per-step value is "
+              f"extrapolated linearly per token" if done < w.batch else
+              f"oracle DELTA-stack step (gather + {len(roles)} layers) of all {w.batch} "
+              f"sequence(s), {spent:.1f} s")
     # oracle seconds per (sequence, layer) for each role, on sequence 0's first layer
     host = synth.sequence_pages(inp, 0, 0)
     s0 = inp.seq_lens_host[0]
