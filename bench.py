@@ -355,7 +355,7 @@ def emit(rec):
 
 def sweep_rounds(D, w, args):
     """Per-round attention latency while a batch decodes from 1 token to the workload's length
-    (the analogue of the paper's per-round latency trace, Sec. 5.2): full stack vs DELTA stack
+    (the analogue of the paper's per-round latency trace, Sec. 5.3): full stack vs DELTA stack
     at sampled contexts, and the attention time summed over every round."""
     S = w.max_seq_len
     base = synth.make_inputs(w, "cuda", poison_tail=False)
@@ -390,7 +390,7 @@ def sweep_rounds(D, w, args):
 
 
 def sweep_deltas(D, w, args):
-    """Step time against the number of Delta-layers (Sec. 5.3): at the longest context (the
+    """Step time against the number of Delta-layers (Sec. 6.1): at the longest context (the
     last decoding round) and averaged over all rounds 1..S; the full stack alongside."""
     S = w.max_seq_len
     L = w.n_layers
@@ -427,7 +427,7 @@ def sweep_deltas(D, w, args):
 
 def sweep_kl(D, w, args):
     """DELTA step time over a grid of page budgets K and recency windows L (pages; L < K), at
-    the workload's context (the runtime counterpart of the paper's (K, L) study, Sec. 5.3)."""
+    the workload's context (the runtime counterpart of the paper's (K, L) study, Sec. 6.2)."""
     import dataclasses
     S = w.max_seq_len
     base = synth.make_inputs(w, "cuda", poison_tail=False)

@@ -9,7 +9,7 @@ budgets (Sec. 5.2), scaled down for the 8-page budget of the tiny check so that 
 not trivial.
 
 Workloads 6-8 are the runtime settings of the paper's throughput and Delta-layer-count
-experiments (Sec. 5.2 and Sec. 5.3): a 1k-token budget (K = 64 pages, L = 8 pages), the
+experiments (Sec. 5.3 and Sec. 6.1): a 1k-token budget (K = 64 pages, L = 8 pages), the
 model-specific Delta-layer sets of Sec. 5, and the batch and maximum decoding length quoted
 for each model.  The paper runs the 7B and 14B models with tensor parallelism over 2 and 4
 GPUs; those workloads hold one GPU's share of the attention heads (the KV heads split evenly
@@ -51,7 +51,7 @@ def roles_for(n_layers: int, delta_layers) -> list:
 
 
 def spread_delta_layers(n_layers: int, count: int, first: int = 2) -> list:
-    """`count` Delta-layers for a sweep over their number (Sec. 5.3): the first at layer
+    """`count` Delta-layers for a sweep over their number (Sec. 6.1): the first at layer
     `first`, the others evenly spaced over the layers after it, up to every layer from
     `first` on."""
     span = n_layers - 1 - first

@@ -80,7 +80,7 @@ def test_shape_validation(D, kw, status):
 
 
 @pytest.mark.parametrize("sel,status", [
-    ((2048, 2048), -1),                # L >= K (Sec. 5 requires L < K)
+    ((2048, 2048), -1),                # L >= K (only L < K is valid, App. C)
     ((2048, 4096), -1),
     ((2040, 128), -1),                 # budget not a whole number of pages
     ((2048, 120), -1),                 # window not a whole number of pages
