@@ -105,6 +105,52 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _dev(name, t, dtype=None, shape=None, at_least=None):
+    """The library reads and writes these buffers on the GPU: refuse, before any launch, a
+    host tensor, a wrong element type, a non-contiguous view or a wrong shape (None entries of
+    `shape` are free; `at_least` bounds the element count instead)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a GPU tensor (got device {t.device})")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if shape is not None and (t.dim() != len(shape) or
+                              any(w is not None and w != d for w, d in zip(shape, t.shape))):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if at_least is not None and t.numel() < at_least:
+        raise ValueError(f"{name}: needs at least {at_least} elements, has {t.numel()}")
+    return t
+
+
+def _check_kv(kv, shape):
+    t = getattr(kv, "_tensors", None)
+    if t is None:   # built by hand from raw pointers: nothing to check
+        return
+    k, v, pt, sl = t
+    cache = (None, shape.n_kv_heads, shape.page_size, shape.head_dim)
+    _dev("k_cache", k, torch.bfloat16, cache)
+    _dev("v_cache", v, torch.bfloat16, cache)
+    _dev("page_table", pt, torch.int32, (shape.batch, shape.max_pages_per_seq))
+    _dev("seq_lens", sl, torch.int32, (shape.batch,))
+
+
+def _check_qo(shape, q, out):
+    qo = (shape.batch, shape.n_q_heads, shape.head_dim)
+    _dev("q", q, torch.bfloat16, qo)
+    _dev("out", out, torch.bfloat16, qo)
+
+
+def _check_sel(shape, sel, sel_idx, sel_cnt, sel_phys=None):
+    K = sel.budget_tokens // max(sel.unit_tokens, 1)
+    _dev("sel_idx", sel_idx, torch.int32, (shape.batch, K))
+    _dev("sel_cnt", sel_cnt, torch.int32, (shape.batch,))
+    if sel_phys is not None:
+        _dev("sel_phys", sel_phys, torch.int32, (shape.batch, K))
+
+
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -120,7 +166,12 @@ def make_select(budget_tokens, recent_tokens, unit_tokens=16, agg=DELTA_AGG_MAX)
 
 
 def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
-    return delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr())
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("page_table", page_table),
+                    ("seq_lens", seq_lens)):
+        _dev(name, t)
+    kv = delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr())
+    kv._tensors = (k_cache, v_cache, page_table, seq_lens)   # checked against the shape per call
+    return kv
 
 
 def delta_workspace_bytes(shape: delta_shape_t, sel: delta_select_t | None = None) -> int:
@@ -132,6 +183,7 @@ def delta_workspace_bytes(shape: delta_shape_t, sel: delta_select_t | None = Non
 
 
 def delta_workspace_init(ws: torch.Tensor):
+    _dev("ws", ws)
     _check("delta_workspace_init", _lib.delta_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream()))
 
 
@@ -145,12 +197,22 @@ def _nbytes(t):
 
 
 def delta_full_attn(shape, kv: delta_kv_t, q, out, ws):
+    _check_kv(kv, shape)
+    _check_qo(shape, q, out)
+    _dev("ws", ws)
     _check("delta_full_attn", _lib.delta_full_attn(ctypes.byref(shape), ctypes.byref(kv), _ptr(q),
                                                    _ptr(out), _ptr(ws), _nbytes(ws), _stream()))
 
 
 def delta_delta_attn_select(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, unit_scores, ws,
                             sel_phys=None):
+    _check_kv(kv, shape)
+    _check_qo(shape, q, out)
+    _check_sel(shape, sel, sel_idx, sel_cnt, sel_phys)
+    if unit_scores is not None:
+        n_u = -(-shape.max_seq_len // max(sel.unit_tokens, 1))
+        _dev("unit_scores", unit_scores, torch.float32, at_least=shape.batch * n_u)
+    _dev("ws", ws)
     _check("delta_delta_attn_select",
            _lib.delta_delta_attn_select(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
                                         ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt),
@@ -159,6 +221,10 @@ def delta_delta_attn_select(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt
 
 
 def delta_sparse_attn(shape, kv: delta_kv_t, q, out, sel, sel_idx, sel_cnt, ws, sel_phys=None):
+    _check_kv(kv, shape)
+    _check_qo(shape, q, out)
+    _check_sel(shape, sel, sel_idx, sel_cnt, sel_phys)
+    _dev("ws", ws)
     _check("delta_sparse_attn",
            _lib.delta_sparse_attn(ctypes.byref(shape), ctypes.byref(kv), _ptr(q), _ptr(out),
                                   ctypes.byref(sel), _ptr(sel_idx), _ptr(sel_cnt), _ptr(sel_phys),
@@ -170,6 +236,20 @@ class StepArgs:
 
     def __init__(self, shape, roles, kvs, qs, outs, sel, sel_idx, sel_cnt, ws):
         n = len(roles)
+        if not (len(kvs) == len(qs) == len(outs) == n):
+            raise ValueError(f"{n} roles need {n} kv, q and out entries "
+                             f"(got {len(kvs)}, {len(qs)}, {len(outs)})")
+        for kv, q, o in zip(kvs, qs, outs):
+            _check_kv(kv, shape)
+            _check_qo(shape, q, o)
+        n_delta = sum(1 for r in roles if r == DELTA_ROLE_DELTA)
+        if n_delta:
+            K = sel.budget_tokens // max(sel.unit_tokens, 1)
+            _dev("sel_idx", sel_idx, torch.int32, (None, shape.batch, K))
+            _dev("sel_cnt", sel_cnt, torch.int32, (None, shape.batch))
+            if sel_idx.shape[0] < n_delta or sel_cnt.shape[0] < n_delta:
+                raise ValueError(f"sel_idx / sel_cnt need a slot for each of the {n_delta} Delta layers")
+        _dev("ws", ws)
         self.shape = shape
         self.n = n
         self.roles = (ctypes.c_int32 * n)(*roles)
@@ -191,6 +271,10 @@ def delta_decode_step(args: StepArgs):
 
 
 def delta_kv_append(shape, k_cache, v_cache, page_table, seq_lens, k_new, v_new):
+    _check_kv(make_kv(k_cache, v_cache, page_table, seq_lens), shape)
+    row = (shape.batch, shape.n_kv_heads, shape.head_dim)
+    _dev("k_new", k_new, torch.bfloat16, row)
+    _dev("v_new", v_new, torch.bfloat16, row)
     _check("delta_kv_append",
            _lib.delta_kv_append(ctypes.byref(shape), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
                                 _ptr(seq_lens), _ptr(k_new), _ptr(v_new), _stream()))

@@ -165,3 +165,28 @@ def test_append_and_hooked_step_reject_before_launch(D):
                                         16, None, P(hooks.c)) == -3
     assert calls == []
     assert D.delta_status_string(-5) == "a layer hook stopped the step"
+
+
+def test_binding_refuses_host_and_mistyped_buffers(D):
+    """The binding checks every tensor it hands to the library before any launch: host
+    memory, a wrong element type, a non-contiguous view or a wrong shape never reaches it."""
+    import torch
+    k = torch.zeros((4, 2, 16, 64), dtype=torch.bfloat16)
+    pt = torch.zeros((1, 4), dtype=torch.int32)
+    sl = torch.ones((1,), dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        D.make_kv(k, k, pt, sl)
+    with pytest.raises(TypeError):
+        D.make_kv(k.numpy(), k, pt, sl)
+    # the per-call checks, on a descriptor built by hand (no tensors attached: skipped) and on
+    # the q / out / selection buffers, which are always checked
+    s = D.make_shape(1, 8, 2, 64, 4, 64)
+    sel = D.make_select(32, 16)
+    kv = D.delta_kv_t(1, 2, 3, 4)
+    q = torch.zeros((1, 8, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        D.delta_full_attn(s, kv, q, q, torch.zeros(16, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        D._dev("q", q, torch.float32)
+    with pytest.raises(ValueError):
+        D._check_sel(s, sel, torch.zeros((1, 3), dtype=torch.int32), torch.zeros((1,), dtype=torch.int32))
