@@ -249,9 +249,12 @@ def test_graph_replay_matches_eager():
 
 
 # ------------------------------------------------------------------------------------------
-# Full-size configs 3-5: the launch configuration the benchmark times, sampled sequences
+# Full-size workloads 3-8: the launch configuration the benchmark and its sweeps time,
+# sampled sequences (6-8: the Qwen-1.5B, Qwen-7B-rank and Qwen-14B-rank runtime settings at
+# batch 64 / 64 / 32 and 16-19K tokens, with the paper's Delta-layer sets)
 # ------------------------------------------------------------------------------------------
-@pytest.mark.parametrize("cfg,seqs", [(3, [0, 9]), (4, [0, 5]), (5, [0, 17, 31])])
+@pytest.mark.parametrize("cfg,seqs", [(3, [0, 9]), (4, [0, 5]), (5, [0, 17, 31]), (6, [0, 63]),
+                                      (7, [1, 40]), (8, [0, 31])])
 def test_full_size_sampled(cfg, seqs):
     inp = _inputs(cfg)
     w = inp.workload
