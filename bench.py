@@ -389,6 +389,128 @@ def sweep_rounds(D, w, args):
           "first_round_us": {"full": round(full_pts[0][1], 2), "delta": round(delta_pts[0][1], 2)}})
 
 
+class SyntheticDecoder:
+    """A decoder with random bf16 weights in the published Qwen2.5-1.5B layout (hidden 1536,
+    12 query / 2 KV heads of 128, MLP 8960, vocabulary 151936), wrapped around the attention
+    path through delta_decode_step_hooked: before each layer's attention a hook applies the
+    RMSNorm and the QKV projection, writes the layer's query and appends the new key and value
+    (delta_kv_append, Eq. kv_update); after it, the output projection, the residual, the second
+    RMSNorm and the gated MLP.  The round ends with the final norm, the LM head and an argmax.
+    Rotary embeddings and projection biases are left out (elementwise work, under 1 % of a
+    round).  Everything runs on the step's stream, so a whole round captures into one graph."""
+
+    def __init__(self, D, w, seed=0):
+        hid, inter, vocab = 1536, 8960, 151936
+        assert (w.n_q_heads * w.head_dim, w.n_kv_heads) == (hid, 2), "Qwen-1.5B attention shape"
+        g = torch.Generator(device="cuda").manual_seed(seed)
+        dev, bf = "cuda", torch.bfloat16
+
+        def rnd(n_out, n_in):   # [out, in], the layout linear layers keep their weights in
+            return (torch.randn((n_out, n_in), generator=g, device=dev) / math.sqrt(n_in)).to(bf)
+        L = w.n_layers
+        kvd = w.n_kv_heads * w.head_dim
+        self.D, self.w = D, w
+        self.wqkv = [rnd(hid + 2 * kvd, hid) for _ in range(L)]
+        self.wo = [rnd(hid, hid) for _ in range(L)]
+        self.wgu = [rnd(2 * inter, hid) for _ in range(L)]
+        self.wd = [rnd(hid, inter) for _ in range(L)]
+        self.ln1 = [torch.ones(hid, dtype=bf, device=dev) for _ in range(L)]
+        self.ln2 = [torch.ones(hid, dtype=bf, device=dev) for _ in range(L)]
+        self.lnf = torch.ones(hid, dtype=bf, device=dev)
+        self.emb = rnd(vocab, hid)
+        self.lm = rnd(vocab, hid)
+        self.tokens = torch.randint(0, vocab, (w.batch,), generator=g, device=dev)
+        self.x = torch.empty((w.batch, hid), dtype=bf, device=dev)
+        self.k_new = torch.empty((w.batch, w.n_kv_heads, w.head_dim), dtype=bf, device=dev)
+        self.v_new = torch.empty_like(self.k_new)
+        self.next = torch.empty((w.batch,), dtype=torch.int64, device=dev)
+        self.hid, self.inter, self.kvd = hid, inter, kvd
+
+    @staticmethod
+    def rmsnorm(x, wt, eps=1e-6):
+        return torch.nn.functional.rms_norm(x, (x.shape[-1],), wt, eps)
+
+    def hooks(self, inp, outs, shape):
+        w, hid, kvd, D = self.w, self.hid, self.kvd, self.D
+
+        def before(i):
+            if i == 0:
+                self.x.copy_(self.emb.index_select(0, self.tokens))
+            lin = torch.nn.functional.linear
+            qkv = lin(self.rmsnorm(self.x, self.ln1[i]), self.wqkv[i])
+            inp.q[i].view(w.batch, hid).copy_(qkv[:, :hid])
+            self.k_new.view(w.batch, kvd).copy_(qkv[:, hid:hid + kvd])
+            self.v_new.view(w.batch, kvd).copy_(qkv[:, hid + kvd:])
+            D.delta_kv_append(shape, inp.k_cache[i], inp.v_cache[i], inp.page_table,
+                              inp.seq_lens, self.k_new, self.v_new)
+
+        def after(i):
+            lin = torch.nn.functional.linear
+            self.x += lin(outs[i].view(w.batch, hid), self.wo[i])
+            gu = lin(self.rmsnorm(self.x, self.ln2[i]), self.wgu[i])
+            self.x += lin(torch.nn.functional.silu(gu[:, :self.inter]) * gu[:, self.inter:], self.wd[i])
+            if i == w.n_layers - 1:
+                logits = lin(self.rmsnorm(self.x, self.lnf), self.lm)
+                self.next.copy_(logits.argmax(-1))
+
+        return D.LayerHooks(before=before, after=after)
+
+
+def sweep_e2e(D, w, args):
+    """Whole decoding rounds of a synthetic-weight Qwen-1.5B-shaped model (SyntheticDecoder)
+    around the attention path, full attention vs DELTA, over the per-round trace of the
+    paper's throughput experiment (Sec. 5.3): per-round latency at sampled contexts, the
+    decoding time summed over all rounds, and the throughput."""
+    S = w.max_seq_len
+    base = synth.make_inputs(w, "cuda", poison_tail=False)
+    torch.cuda.synchronize()
+    sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX)
+    ws = D.alloc_workspace(D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                        base.max_pages_per_seq, S), sel)
+    ctx = sorted({1, 512, w.budget_tokens, w.budget_tokens + configs.PAGE,
+                  *range(2048, S + 1, 2048), S})
+    kv_tok = 4 * w.n_kv_heads * w.head_dim
+    pts = {"full": [], "delta": []}
+    model = SyntheticDecoder(D, w)
+    for s in ctx:
+        shape = D.make_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                             base.max_pages_per_seq, s)
+        sets = context_sets(base, s, w.batch * kv_tok * step_tokens(w, w.roles, s))
+        res = {}
+        for name, roles in (("full", [configs.ROLE_FULL] * w.n_layers), ("delta", w.roles)):
+            D.delta_workspace_init(ws)
+            st = Stack(D, w, sets, roles, shape, sel, ws)
+            graphs = []
+            for k, inp in enumerate(sets):
+                hooks = model.hooks(inp, st.outs[k], shape)
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    D.delta_decode_step_hooked(st.args[k], hooks)
+                torch.cuda.current_stream().wait_stream(side)
+                torch.cuda.synchronize()
+                gr = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gr):
+                    D.delta_decode_step_hooked(st.args[k], hooks)
+                graphs.append(gr)
+            st.graphs = graphs
+            res[name] = time_steps(st, args.steps, args.warmup) * 1e3
+            del st, graphs
+        for name in pts:
+            pts[name].append((s, res[name]))
+        emit({"mode": "e2e", "workload": w.name, "context": s, "full_round_us": round(res["full"], 2),
+              "delta_round_us": round(res["delta"], 2), "input_copies_rotated": len(sets)})
+        torch.cuda.empty_cache()
+    tf, td = trapezoid_rounds(pts["full"]), trapezoid_rounds(pts["delta"])
+    emit({"mode": "e2e-summary", "workload": w.describe(), "model": "synthetic Qwen2.5-1.5B layout",
+          "rounds": S, "delta_layers": w.delta_layers,
+          "decode_s_all_rounds": {"full": round(tf, 3), "delta": round(td, 3)},
+          "tokens_per_s": {"full": round(w.batch * S / tf, 1), "delta": round(w.batch * S / td, 1)},
+          "speedup": round(tf / td, 3),
+          "first_round_us": {"full": round(pts["full"][0][1], 1), "delta": round(pts["delta"][0][1], 1)},
+          "last_round_us": {"full": round(pts["full"][-1][1], 1), "delta": round(pts["delta"][-1][1], 1)}})
+
+
 def sweep_deltas(D, w, args):
     """Step time against the number of Delta-layers (Sec. 6.1): at the longest context (the
     last decoding round) and averaged over all rounds 1..S; the full stack alongside."""
@@ -657,7 +779,7 @@ def main():
                     help="workload (default 3; the sweeps default to the paper's model for them)")
     ap.add_argument("--delta-layers", type=str, default=None,
                     help="comma-separated Delta-layer indices replacing the workload's schedule")
-    ap.add_argument("--sweep", choices=["rounds", "deltas", "kl", "overhead", "append"], default=None,
+    ap.add_argument("--sweep", choices=["rounds", "deltas", "kl", "overhead", "append", "e2e"], default=None,
                     help="print one JSON line per point of a runtime sweep instead of the "
                          "headline measurement")
     ap.add_argument("--unit-tokens", type=int, default=16, choices=[16, 1])
@@ -671,7 +793,7 @@ def main():
     from paper_2510_09883_amd import delta as D
 
     if args.sweep is not None:
-        default = {"rounds": 6, "deltas": 6, "kl": 7, "overhead": None, "append": 3}[args.sweep]
+        default = {"rounds": 6, "deltas": 6, "kl": 7, "overhead": None, "append": 3, "e2e": 6}[args.sweep]
         w = configs.get(args.config or default, args.unit_tokens) if default else None
         if w is not None and args.delta_layers:
             w.set_delta_layers(args.delta_layers.split(","))
@@ -679,7 +801,7 @@ def main():
             log(f"sweep {args.sweep}: {w.describe()}")
         {"rounds": lambda: sweep_rounds(D, w, args), "deltas": lambda: sweep_deltas(D, w, args),
          "kl": lambda: sweep_kl(D, w, args), "overhead": lambda: sweep_overhead(D, args),
-         "append": lambda: sweep_append(D, w, args)}[args.sweep]()
+         "append": lambda: sweep_append(D, w, args), "e2e": lambda: sweep_e2e(D, w, args)}[args.sweep]()
         return
 
     w = configs.get(args.config or 3, args.unit_tokens)
