@@ -49,3 +49,21 @@ def test_remaining_group_sizes(hq, hkv, d):
     w, inp = _tiny([900, 2000], n_q_heads=hq, n_kv_heads=hkv, head_dim=d)
     res = run_step(inp)
     check_step(inp, res).assert_ok()
+
+
+def test_workspace_moves_between_shapes_after_init():
+    """One workspace, sized for the larger call, serves calls of two different shapes (batch,
+    context and budget) after delta_workspace_init, as the runtime sweeps use it."""
+    from gpu_helpers import D, shape_of, select_of
+    d = D()
+    w1, inp1 = _tiny([3000, 900, 17])
+    w2, inp2 = _tiny([5000, 2000], budget=256, recent_pages=2, n_q_heads=16, n_kv_heads=4,
+                     head_dim=128)
+    big = max(d.delta_workspace_bytes(shape_of(i), select_of(w)) for i, w in ((inp1, w1), (inp2, w2)))
+    ws = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    for rnd in range(2):
+        for w, inp in ((w1, inp1), (w2, inp2)):
+            d.delta_workspace_init(ws)
+            res = run_step(inp, ws=ws, budget=w.budget_tokens, recent=w.recent_tokens)
+            check_step(inp, res, budget=w.budget_tokens, recent=w.recent_tokens).assert_ok()
+    log("workspace reuse across shapes ok")
