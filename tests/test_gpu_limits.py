@@ -67,3 +67,15 @@ def test_workspace_moves_between_shapes_after_init():
             res = run_step(inp, ws=ws, budget=w.budget_tokens, recent=w.recent_tokens)
             check_step(inp, res, budget=w.budget_tokens, recent=w.recent_tokens).assert_ok()
     log("workspace reuse across shapes ok")
+
+
+def test_large_batch_of_short_ragged_sequences():
+    """512 sequences of 1..600 tokens (one to 38 pages, most shorter than the 8-page budget
+    or just above it): many small (sequence, KV head) pairs and selection workgroups."""
+    g = torch.Generator().manual_seed(512)
+    lens = torch.randint(1, 601, (512,), generator=g).tolist()
+    w, inp = _tiny(lens)
+    res = run_step(inp)
+    check_step(inp, res, seqs=list(range(0, 512, 7)) + [511]).assert_ok()
+    cnt = res.sel_cnt[0].cpu().tolist()
+    assert cnt == [min(w.budget_units, (s + 15) // 16) for s in lens]
