@@ -232,6 +232,7 @@ bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const La
   if (s->head_dim != 128 || s->n_kv_heads % 4 != 0 || s->n_q_heads > kFusedMaxQHeads) return false;
   const int n_c = L.nu_stride - sel->recent_tokens / sel->unit_tokens;
   if (n_c > kFusedKeysPerThread * 256) return false;
+  if (L.fused_chunks > kFusedMaxChunks) return false;
   const int64_t grid = (int64_t)L.fused_chunks * s->batch;
   const int64_t part_bytes = (int64_t)s->batch * s->n_q_heads * L.fused_chunks * s->head_dim * 4;
   if (part_bytes > 0x7fffffff) return false;

@@ -22,6 +22,8 @@
 // workgroup ever waits without a bound.  When every workgroup is resident the logits never
 // reach HBM; the split path (attention kernel + score kernel + select kernel) writes and
 // re-reads them.
+#include <type_traits>
+
 #include "attn_tile.h"
 #include "internal.h"
 #include "select_impl.h"
@@ -149,66 +151,76 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
   const bool ok = s_ok != 0;
 
   // ---- 3. log-sum-exp of every query head ------------------------------------------------
-  // (max, sum) of the chunk partials, folded kBatch chunks at a time with all of a batch's loads
-  // in flight, in chunk order
-  constexpr int kBatch = 16;
-  auto compute_lse = [&]() {
+  // (max, sum) of the chunk partials in chunk order, all n_active loads in flight at once
+  // (n_active <= kFusedMaxChunks).  lse_heads is the work of threads tid < Hq; compute_lse
+  // adds the barrier that publishes s_M, s_L and s_lse.
+  constexpr int kNc = kFusedMaxChunks;
+  auto lse_heads = [&]() {
     if (tid < Hq) {
       const int g = tid / G, h = tid - (tid / G) * G;
       const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;   // chunk cc: row0 + cc * G
-      float M = kNegInfF, L = 0.f;
-      for (int c0 = 0; c0 < n_active; c0 += kBatch) {
-        float2 ml[kBatch];
+      float2 ml[kNc];
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i) ml[i] = load_ml(rml, (row0 + min(c0 + i, n_active - 1) * G) * 8);
-        float bm = kNegInfF;
+      for (int i = 0; i < kNc; ++i) ml[i] = load_ml(rml, (row0 + min(i, n_active - 1) * G) * 8);
+      float M = kNegInfF;
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i)
-          if (c0 + i < n_active) bm = fmaxf(bm, ml[i].x);
-        const float Mn = fmaxf(M, bm);
-        const float Mu = (Mn == kNegInfF) ? 0.f : Mn;
-        L *= exp2f(M - Mu);
+      for (int i = 0; i < kNc; ++i)
+        if (i < n_active) M = fmaxf(M, ml[i].x);
+      const float Mu = (M == kNegInfF) ? 0.f : M;
+      float L = 0.f;
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i)
-          if (c0 + i < n_active) L += (ml[i].x == kNegInfF ? 0.f : exp2f(ml[i].x - Mu)) * ml[i].y;
-        M = Mn;
-      }
+      for (int i = 0; i < kNc; ++i)
+        if (i < n_active) L += (ml[i].x == kNegInfF ? 0.f : exp2f(ml[i].x - Mu)) * ml[i].y;
       s_M[tid] = M;
       s_L[tid] = L;
       s_lse[tid] = M + log2f(L);
     }
+  };
+  auto compute_lse = [&]() {
+    lse_heads();
     __syncthreads();
   };
 
   // ---- 4. outputs of heads cc, cc + n_active, ... (chunk order: deterministic) -----------
-  auto merge_outputs = [&](int cc) {
-    constexpr int kQuads = D / 4;                       // threads per head
-    constexpr int kHeadsAtOnce = kAttnThreads / kQuads;
-    const int dc = 4 * (tid % kQuads);
-    for (int j = cc + n_active * (tid / kQuads); j < Hq; j += n_active * kHeadsAtOnce) {
-      const int g = j / G, h = j - (j / G) * G;
+  // Waves 1-3 merge, kQuads threads per head; each pass issues all of its partial loads at
+  // once.  mid() runs on every thread once, after the first pass's loads are issued and before
+  // they are used: it must leave s_M and s_L published (the log-sum-exp of step 3).
+  auto merge_outputs = [&](int cc, auto&& mid) {
+    constexpr int kQuads = D / 4;                            // threads per head
+    constexpr int kPassHeads = (kAttnThreads - 64) / kQuads;
+    const int mt = tid - 64;                                  // merge thread, waves 1-3
+    const int dc = 4 * (max(mt, 0) % kQuads);
+    const int n_heads = cc < Hq ? (Hq - cc + n_active - 1) / n_active : 0;
+    const int n_pass = max(1, (n_heads + kPassHeads - 1) / kPassHeads);   // uniform
+    for (int pass = 0; pass < n_pass; ++pass) {
+      const int j = mt >= 0 ? cc + n_active * (pass * kPassHeads + mt / kQuads) : Hq;
+      const bool act = j < Hq;
+      const int g = act ? j / G : 0, h = act ? j - (j / G) * G : 0;
       const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;
-      const float Mj = s_M[j];
-      f32x4 O = {0.f, 0.f, 0.f, 0.f};
-      for (int c0 = 0; c0 < n_active; c0 += kBatch) {
-        float m[kBatch];
-        f32x4 ov[kBatch];
+      float m[kNc];
+      f32x4 ov[kNc];
+      if (act) {
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i) {
-          const int row = row0 + min(c0 + i, n_active - 1) * G;
+        for (int i = 0; i < kNc; ++i) {
+          const int row = row0 + min(i, n_active - 1) * G;
           m[i] = load_ml(rml, row * 8).x;
           ov[i] = __builtin_bit_cast(
               f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, (row * D + dc) * 4, 0, kCoherent));
         }
-#pragma unroll
-        for (int i = 0; i < kBatch; ++i)
-          if (c0 + i < n_active) O += (m[i] == kNegInfF ? 0.f : exp2f(m[i] - Mj)) * ov[i];
       }
-      const float lsum = s_L[j];
-      uint2 packed;
-      packed.x = (uint32_t)f32_to_bf16_rne(O[0] / lsum) | ((uint32_t)f32_to_bf16_rne(O[1] / lsum) << 16);
-      packed.y = (uint32_t)f32_to_bf16_rne(O[2] / lsum) | ((uint32_t)f32_to_bf16_rne(O[3] / lsum) << 16);
-      *reinterpret_cast<uint2*>(a.out + ((size_t)b * Hq + j) * D + dc) = packed;
+      if (pass == 0) mid();
+      if (act) {
+        const float Mj = s_M[j];
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < kNc; ++i)
+          if (i < n_active) O += (m[i] == kNegInfF ? 0.f : exp2f(m[i] - Mj)) * ov[i];
+        const float lsum = s_L[j];
+        uint2 packed;
+        packed.x = (uint32_t)f32_to_bf16_rne(O[0] / lsum) | ((uint32_t)f32_to_bf16_rne(O[1] / lsum) << 16);
+        packed.y = (uint32_t)f32_to_bf16_rne(O[2] / lsum) | ((uint32_t)f32_to_bf16_rne(O[3] / lsum) << 16);
+        *reinterpret_cast<uint2*>(a.out + ((size_t)b * Hq + j) * D + dc) = packed;
+      }
     }
   };
 
@@ -220,33 +232,46 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
     const int k = tid >> 2;           // page of the chunk (kC * 4 == kAttnThreads)
     const int r0 = 4 * (tid & 3);     // its rows r0 .. r0 + 3
     const int t0 = (pc + k) * 16 + r0;
-    float acc[4];
+    // x_j(t) - lse_j folded over the query heads in (KV head, head in group) order; the
+    // reduction (max, or sum of 2^) is fixed at compile time so the loop carries no branch,
+    // and a KV head's G logit reads are issued together
+    auto fold = [&](auto max_mode, float (&acc)[4]) {
+      constexpr bool kMax = decltype(max_mode)::value;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = a.agg == 0 ? kNegInfF : 0.f;
-    if (k < npc) {
+      for (int i = 0; i < 4; ++i) acc[i] = kMax ? kNegInfF : 0.f;
+      if (k >= npc) return;
       for (int g = 0; g < Hkv; ++g) {
         const float* glog = a.logits + (((size_t)b * Hkv + g) * a.logit_pages + pc + k) * G * 16 + r0;
+        f32x4 x[G];
+        float l[G];
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          f32x4 x;
+          l[h] = s_lse[g * G + h];
           if (from_lds) {
-            x = *reinterpret_cast<const f32x4*>(&s_logit[(((size_t)g * kC + k) * G + h) * 16 + r0]);
+            x[h] = *reinterpret_cast<const f32x4*>(&s_logit[(((size_t)g * kC + k) * G + h) * 16 + r0]);
           } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              x[i] = __hip_atomic_load(glog + h * 16 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              x[h][i] = __hip_atomic_load(glog + h * 16 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
-          const float l = s_lse[g * G + h];
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            acc[i] = a.agg == 0 ? fmaxf(acc[i], x[i] - l) : acc[i] + exp2f(x[i] - l);
-        }
+            acc[i] = kMax ? fmaxf(acc[i], x[h][i] - l[h]) : acc[i] + exp2f(x[h][i] - l[h]);
       }
-    }
-    float sc[4];
+    };
+    float acc[4], sc[4];
+    if (a.agg == 0) {
+      fold(std::true_type{}, acc);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      sc[i] = (k < npc && t0 + i < s_b) ? (a.agg == 0 ? exp2f(acc[i]) : acc[i]) : 0.f;
+      for (int i = 0; i < 4; ++i) sc[i] = (k < npc && t0 + i < s_b) ? exp2f(acc[i]) : 0.f;
+    } else {
+      fold(std::false_type{}, acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sc[i] = (k < npc && t0 + i < s_b) ? acc[i] : 0.f;
+    }
     float* S = a.unit_scores + (size_t)b * a.sel.nu_stride;
     if (U == 16) {
       float p = (sc[0] + sc[1]) + (sc[2] + sc[3]);
@@ -264,9 +289,13 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
 
   int32_t* deferred = a.chunk_flags + (size_t)b * a.n_chunks;
   if (ok) {
-    compute_lse();
-    merge_outputs(c);
-    score_chunk(c, true);
+    // the log-sum-exp loads (wave 0) and the first merge pass's loads (waves 1-3) are in flight
+    // together; the chunk is scored before the merge arithmetic, so the page scores leave first
+    merge_outputs(c, [&]() {
+      lse_heads();
+      lds_barrier();   // s_M, s_L, s_lse; the merge loads stay in flight
+      score_chunk(c, true);
+    });
   } else {
     // leave the chunk to the sequence's last workgroup: its logits go to the workspace
     for (int g = 0; g < Hkv; ++g) {
@@ -300,7 +329,7 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
       if (tid == 0) s_flag = __hip_atomic_load(deferred + cc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __syncthreads();
       if (s_flag) {
-        merge_outputs(cc);
+        merge_outputs(cc, []() {});
         score_chunk(cc, false);
         if (tid == 0) __hip_atomic_store(deferred + cc, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }

@@ -75,6 +75,7 @@ hipError_t launch_select(const SelectArgs& a, int batch, hipStream_t stream);
 constexpr int kFusedChunkPages = 64;
 constexpr int kFusedMaxQHeads = 32;      // LDS holds kFusedMaxQHeads x 64 x 16 fp32 logits
 constexpr int kFusedKeysPerThread = 8;   // selection candidates held per thread (2048 units)
+constexpr int kFusedMaxChunks = 32;      // chunks per sequence (2048 pages): partials load at once
 
 struct FusedArgs {
   const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
