@@ -66,7 +66,20 @@ struct SplitPlan {
   int n_split = 0;
   int gps = 0;
   int max_groups = 0;
+  int slots = 0;       // partial slots per (sequence, kv head)
+  int chunk_min = 0;   // balanced decomposition: shortest run
+  int balance = 0;     // balanced decomposition allowed (dense launches)
 };
+
+// Whether dense launches may spread a ragged batch's work evenly (the balanced decomposition
+// of the attention kernel).  DELTA_ATTN_BALANCE=0 keeps the static one, for comparison.
+bool balance_enabled() {
+  static int v = [] {
+    const char* e = getenv("DELTA_ATTN_BALANCE");
+    return e && atoi(e) == 0 ? 0 : 1;
+  }();
+  return v != 0;
+}
 
 // Splits per (sequence, kv head) and groups per split for a launch over at most `max_groups`
 // groups of 16 rows.  Deterministic in the shape, so a FULL and a DELTA call over the same
@@ -83,7 +96,24 @@ bool plan_split(int pairs, int max_groups, int slot_cap, SplitPlan* p) {
   p->n_split = n_split;
   p->gps = gps;
   p->max_groups = max_groups;
+  p->slots = n_split;
   return true;
+}
+
+// The balanced decomposition of a dense launch over `batch` sequences, 2 to kBalanceMaxBatch
+// (one sequence cannot be ragged; the kernel holds one sequence length per lane).  Runs are at
+// least chunk_min groups, so no pair is cut into more than slots pieces, and at most
+// kMaxRowSlots: the run of a workgroup of the static grid, ceil(work / workgroups), never
+// exceeds gps.
+void plan_balance(int batch, int pairs, SplitPlan* p) {
+  const int cap = std::min(max_splits(), kMaxSplits - 1);
+  const int chunk_min = std::max(min_groups_per_split(), ceil_div(p->max_groups, cap));
+  if (!balance_enabled() || batch < 2 || batch > kBalanceMaxBatch || chunk_min > kMaxRowSlots) return;
+  // the kernel does the cut's arithmetic in 32 bits
+  if ((int64_t)pairs * p->max_groups >= ((int64_t)1 << 31)) return;
+  p->chunk_min = chunk_min;
+  p->slots = std::max(p->n_split, ceil_div(p->max_groups, chunk_min) + 1);
+  p->balance = 1;
 }
 
 struct Layout {
@@ -133,7 +163,8 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
   const int G = s->n_q_heads / s->n_kv_heads;
   if (!plan_split(pairs, ceil_div(s->max_seq_len, 16), kMaxRowSlots, &L->dense))
     return DELTA_ERR_UNSUPPORTED;
-  L->max_split = L->dense.n_split;
+  plan_balance(s->batch, pairs, &L->dense);
+  L->max_split = L->dense.slots;
   if (sel) {
     const int K = sel->budget_tokens / sel->unit_tokens;
     if (sel->unit_tokens == 16) {
@@ -144,7 +175,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
       if (!plan_split(pairs, ceil_div(K, 16), kMaxRowSlots / 16, &L->sparse))
         return DELTA_ERR_UNSUPPORTED;
     }
-    L->max_split = std::max(L->max_split, L->sparse.n_split);
+    L->max_split = std::max(L->max_split, L->sparse.slots);
     // the selection holds the older units of one sequence in one workgroup's registers
     if (ceil_div(s->max_seq_len, sel->unit_tokens) - sel->recent_tokens / sel->unit_tokens > kMaxSelectKeys)
       return DELTA_ERR_UNSUPPORTED;
@@ -204,6 +235,9 @@ AttnArgs base_args(const delta_shape_t* s, const delta_kv_t* kv, const void* q, 
   a.n_split = plan.n_split;
   a.gps = plan.gps;
   a.max_groups = plan.max_groups;
+  a.slots = plan.slots;
+  a.chunk_min = plan.chunk_min;
+  a.balance = plan.balance;
   a.scale_log2 = scale_log2(s);
   return a;
 }

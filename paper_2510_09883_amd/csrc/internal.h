@@ -19,6 +19,7 @@ constexpr int kMaxSplits = 64;           // split partials combined by the last 
 constexpr int kMaxRowSlots = 1024;       // LDS slots staging a split's page / row list
 constexpr int kMaxGroup = 8;             // query heads per KV head (padded to 16 MFMA columns)
 constexpr int kMaxSelectKeys = 8192;     // candidate units one selection workgroup holds in registers
+constexpr int kBalanceMaxBatch = 64;     // sequences of a balanced dense launch (one per lane)
 
 struct AttnArgs {
   const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
@@ -30,15 +31,19 @@ struct AttnArgs {
   const int32_t* sel_phys;   // [B, sel_stride] physical locations of sel_idx, or null
   const uint16_t* q;         // bf16 [B, Hq, D]
   uint16_t* out;             // bf16 [B, Hq, D]
-  float* part_o;             // [B*Hkv, n_split, G, D]   un-normalised split outputs
-  float* part_ml;            // [B*Hkv, n_split, G, 2]   split (max, sum) in the log2 domain
+  float* part_o;             // [B*Hkv, slots, G, D]   un-normalised partial outputs
+  float* part_ml;            // [B*Hkv, slots, G, 2]   partial (max, sum) in the log2 domain
   int32_t* counters;         // [B*Hkv] arrival counters, zero between launches
   float* logits;             // [B, Hkv, logit_pages, G, 16] log2-domain logits, or null
   float* lse;                // [B, Hq] log2-domain log-sum-exp, or null
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
   int32_t n_q_heads, n_kv_heads, max_pages, sel_stride, logit_pages;
-  int32_t n_split, gps;      // splits per (b, kv head) and 16-row groups per split
+  int32_t n_split, gps;      // static decomposition: splits per (b, kv head), 16-row groups
+                             // per split; the grid is (n_split, Hkv, B)
   int32_t max_groups;        // host bound on groups per sequence (n_split * gps >= it)
+  int32_t slots;             // partial slots per (b, kv head), >= the pieces of any pair
+  int32_t chunk_min;         // shortest run of the balanced decomposition (dense launches)
+  int32_t balance;           // 1: a dense launch may take the balanced decomposition
   float scale_log2;          // sm_scale * log2(e)
 };
 

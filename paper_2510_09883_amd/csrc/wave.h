@@ -52,8 +52,9 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Bitwise OR / AND of all 64 lanes, returned in every lane (quad swaps, row half-mirror and
-// mirror, then the 16- and 32-lane swaps; OR and AND are idempotent, so any pairing works).
+// Bitwise OR / AND and unsigned minimum of all 64 lanes, returned in every lane (quad swaps,
+// row half-mirror and mirror, then the 16- and 32-lane swaps; the three operations are
+// idempotent, so any pairing works).
 __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
   v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xf, 0xf, false);
   v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xf, 0xf, false);
@@ -73,6 +74,17 @@ __device__ __forceinline__ uint32_t wave_and(uint32_t v) {
   v = p[0] & p[1];
   const auto q = __builtin_amdgcn_permlane32_swap(v, v, false, false);
   return q[0] & q[1];
+}
+
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xf, 0xf, false));
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xf, 0xf, false));
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xf, 0xf, false));
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xf, 0xf, false));
+  const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = min(p[0], p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return min(q[0], q[1]);
 }
 
 // Workgroup barrier that orders LDS accesses only: the waves wait for their own LDS operations,
