@@ -859,7 +859,9 @@ def main():
                    "sparse": "attn_kernel (selected pages)"}[dominant]
     mode = {"full": 0, "delta": 0, "sparse": 1 if w.unit_tokens == 16 else 2}[dominant]
     logits = "true" if dominant == "delta" else "false"
-    kernel_tag = f"attn_kernel<{w.head_dim}, {w.group}, {mode}, {logits}>"
+    # dense launches over 2-64 sequences run the balanced instantiation
+    balanced = "true" if mode == 0 and 2 <= w.batch <= 64 else "false"
+    kernel_tag = f"attn_kernel<{w.head_dim}, {w.group}, {mode}, {logits}, {balanced}>"
     traffic = measured_traffic(dominant, w, kernel_tag)
     achieved = role_bytes[dominant] / (layer_us[dominant] * 1e-6) / 1e9
     overhead = (layer_us["delta"] - layer_us["full"]) / layer_us["full"] if "delta" in layer_us and "full" in layer_us else None
