@@ -34,6 +34,11 @@
  *             identical outputs, and a DELTA layer's attention output is bitwise identical to
  *             delta_full_attn's on the same inputs (with the optional fused DELTA kernel, see
  *             delta_delta_attn_select, the two agree up to floating-point summation order).
+ *             FULL and DELTA calls over 2 to 64 sequences split the batch's work evenly over
+ *             the GPU from the actual sequence lengths, so a sequence's output bits (never
+ *             its accuracy) can depend on the other sequences' lengths in the same call;
+ *             DELTA_ATTN_BALANCE=0 in the environment (read once per process) keeps the
+ *             per-sequence split, whose bits depend on the sequence and the shape only.
  *   Workspace. `ws` is caller-owned device memory of at least delta_workspace_bytes() bytes.
  *             It must be zero-filled once after allocation; every call leaves it ready for the
  *             next call with the same shape and selection parameters.  Calls with another
