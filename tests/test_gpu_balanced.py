@@ -7,9 +7,11 @@ Llama-8B attention shape, six sequences of 1.8K-4K tokens: the launch has 288 wo
 pairs (113 to 256 groups) are each combined from 5 to 10 pieces cut at places that do not
 depend on the pair.  Qwen-7B shape with sequences of 77-120 tokens: runs of 8 groups over pairs
 of 5-8, so one run holds a whole pair (written directly, no combine) and parts of its
-neighbours.  Outputs and selections are checked against the oracle, and the Delta layer's
-output against the full layer's, bit for bit (App. A, Alg. 1: the Delta layer's attention is
-the full attention).
+neighbours.  Eight seeded random shapes (group sizes 1-8, head dims 64 and 128, 1-8 KV heads,
+2-12 sequences of lengths in [L/2, L], shuffled page tables on odd seeds) cover the other
+kernel instantiations.  Outputs and selections are checked against the oracle, and the Delta
+layer's output against the full layer's, bit for bit (App. A, Alg. 1: the Delta layer's
+attention is the full attention).
 """
 import pytest
 import torch
@@ -62,3 +64,31 @@ def test_balanced_runs_match_oracle(cid, lens):
     for a, b in zip(res.outs, res2.outs):
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     log(f"{w.name}: balanced runs ok")
+
+
+def _random_case(seed):
+    """A seeded random shape (group size 1-8, head dim 64 or 128, 1-8 KV heads, 2-12
+    sequences) with lengths in [L/2, L] (the cut is taken), shuffled pages on odd seeds."""
+    import random
+    r = random.Random(seed)
+    hkv = r.choice([1, 2, 4, 8])
+    G = r.randint(1, 8)
+    d = r.choice([64, 128])
+    B = r.randint(2, 12)
+    L = r.randint(300, 3000)
+    lens = [r.randint(L // 2, L) for _ in range(B)]
+    w = configs.Workload(90 + seed, f"random{seed}", 3, G * hkv, hkv, d, B, max(lens), 256,
+                         hh_frac=0.02, shuffled_pages=bool(seed % 2),
+                         roles=[configs.ROLE_FULL, configs.ROLE_DELTA, configs.ROLE_SPARSE])
+    return w, lens
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_balanced_random_shapes(seed):
+    w, lens = _random_case(seed)
+    log(f"random case {seed}: Hq {w.n_q_heads} Hkv {w.n_kv_heads} d {w.head_dim} lens {lens}")
+    inp = synth.make_inputs(w, "cuda", seq_lens=lens)
+    torch.cuda.synchronize()
+    res = run_step(inp)
+    check_step(inp, res, seqs=sorted({0, len(lens) // 2, len(lens) - 1})).assert_ok()
+    _delta_equals_full(w, inp)
