@@ -11,10 +11,10 @@
 // D = 128, contiguous in HBM), or 16 gathered token rows in token-level sparse mode.  The grid
 // is (split, kv head g, sequence b), 4 waves per workgroup.  Statically, workgroup (split, g,
 // b) takes the run of `gps` groups starting at split * gps of pair (b, g).  A dense launch
-// (full / Delta layers) over a ragged batch instead cuts the batch's actual groups, in (b, g,
-// page) order, into equal runs, one per workgroup, each run possibly spanning pairs, so that
-// every CU gets the same work whatever the spread of sequence lengths; with equal lengths the
-// two cuts coincide.  Waves take a piece's groups in interleaved blocks of four and keep their
+// (full / Delta layers) over a ragged batch of 2-64 sequences instead cuts the batch's actual
+// groups, in (b, g, page) order, into equal runs, one per workgroup, each run possibly
+// spanning pairs, so that every CU gets the same work whatever the spread of sequence
+// lengths; with equal lengths the two cuts coincide.  Waves take a piece's groups in interleaved blocks of four and keep their
 // own online-softmax state; all G query heads of the KV group share every K/V byte read.
 //
 // Per group and wave:
@@ -100,7 +100,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       }
     }
   };
-  // nothing to attend to (an empty sequence): defined output (zeros), log-sum-exp = -inf
+  // nothing to attend to (an empty sequence, or no selected unit): defined output (zeros),
+  // log-sum-exp = -inf
   auto write_empty = [&](int b, int g) {
     for (int i = tid; i < G * D; i += kAttnThreads) a.out[((size_t)b * Hq + g * G) * D + i] = 0;
     if (LOGITS && tid < G) a.lse[(size_t)b * Hq + g * G + tid] = kNegInf;
@@ -359,7 +360,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   int bal_w = 0, bal_x = 0, bal_xe = 0;   // this workgroup's run [bal_x, bal_xe)
   // lane l of every wave: sequence l's length, groups, and groups of sequences 0 .. l - 1
   int bal_len = 0, bal_units = 0, bal_before = 0;
-  if (MODE == ROWS_DENSE && BAL) {
+  if (MODE == ROWS_DENSE && BAL && gridDim.z <= 64) {   // one sequence per lane
     // Balanced decomposition of a dense launch (the work of a ragged batch spread evenly):
     // the groups of every (sequence, KV head) pair, in (b, g, page) order, are cut into runs of
     // `chunk` groups, run w for workgroup w (the launch's linear index, in dispatch order).  A
