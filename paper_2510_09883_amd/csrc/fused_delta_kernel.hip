@@ -161,7 +161,10 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
       const int row0 = ((b * Hkv + g) * a.n_chunks) * G + h;   // chunk cc: row0 + cc * G
       float2 ml[kNc];
 #pragma unroll
-      for (int i = 0; i < kNc; ++i) ml[i] = load_ml(rml, (row0 + min(i, n_active - 1) * G) * 8);
+      for (int i = 0; i < kNc; ++i) {   // chunks past the sequence's last are not loaded
+        ml[i] = make_float2(kNegInfF, 0.f);
+        if (i < n_active) ml[i] = load_ml(rml, (row0 + i * G) * 8);
+      }
       float M = kNegInfF;
 #pragma unroll
       for (int i = 0; i < kNc; ++i)
@@ -202,10 +205,14 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
       if (act) {
 #pragma unroll
         for (int i = 0; i < kNc; ++i) {
-          const int row = row0 + min(i, n_active - 1) * G;
-          m[i] = load_ml(rml, row * 8).x;
-          ov[i] = __builtin_bit_cast(
-              f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, (row * D + dc) * 4, 0, kCoherent));
+          m[i] = kNegInfF;
+          ov[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (i < n_active) {
+            const int row = row0 + i * G;
+            m[i] = load_ml(rml, row * 8).x;
+            ov[i] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, (row * D + dc) * 4, 0, kCoherent));
+          }
         }
       }
       if (pass == 0) mid();
