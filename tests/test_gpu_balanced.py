@@ -92,3 +92,22 @@ def test_balanced_random_shapes(seed):
     res = run_step(inp)
     check_step(inp, res, seqs=sorted({0, len(lens) // 2, len(lens) - 1})).assert_ok()
     _delta_equals_full(w, inp)
+
+
+@pytest.mark.parametrize("B", [64, 65])
+def test_balanced_batch_limit(B):
+    """64 sequences fill the lanes of the balanced cut; at 65 the host keeps the static split.
+    Qwen-1.5B attention shape (12/2/128) with lengths in [400, 800]."""
+    import random
+    r = random.Random(B)
+    lens = [r.randint(400, 800) for _ in range(B)]
+    w = configs.get(6)
+    w.batch = B
+    w.n_layers = 3
+    w.set_delta_layers([1])
+    log(f"generating {w.describe()} B={B}")
+    inp = synth.make_inputs(w, "cuda", seq_lens=lens)
+    torch.cuda.synchronize()
+    res = run_step(inp)
+    check_step(inp, res, seqs=[0, 31, B - 2, B - 1]).assert_ok()
+    _delta_equals_full(w, inp)
