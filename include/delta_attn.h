@@ -136,7 +136,9 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  * kernel and a selection kernel.  With DELTA_DELTA_PATH=fused in the environment, shapes with
  * head_dim 128, a multiple of 4 KV heads, at most 32 query heads, at most 2048 candidate units
  * and a grid the device holds at once instead run one kernel that keeps the logits on chip
- * (opt-in: measured on MI355X it is no faster than the split launches).  Its workgroups wait
+ * (opt-in: on MI355X it is faster only where its grid fills the device, e.g. 101 vs 105 us
+ * per layer for 8 sequences of 32K tokens with 28 query and 4 KV heads; its `out` agrees with
+ * delta_full_attn's up to summation order, not bit for bit).  Its workgroups wait
  * for the rest of their sequence for at most DELTA_FUSED_SPIN_TICKS ticks of the 100 MHz clock
  * (default 10 ms) and then hand their part to the sequence's last workgroup, so it never
  * hangs when not all of them are resident, and gives the same results either way. */
@@ -144,6 +146,12 @@ int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, co
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
                             int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,
                             size_t ws_bytes, void* stream);
+
+/* Which path delta_delta_attn_select takes for this shape and selection under the current
+ * environment and device: *fused = 1 for the fused kernel (see above), 0 for the attention,
+ * scoring and selection launches.  Host only; it queries the current device's occupancy for
+ * the fused kernel.  Errors as delta_workspace_bytes; `sel` and `fused` must be non-NULL. */
+int delta_delta_path(const delta_shape_t* shape, const delta_select_t* sel, int* fused);
 
 /* SPARSE role: attention of each query over the tokens of the selected units only, the
  * softmax renormalised over them (App. A, Alg. 1 sparse branch).  Unit u covers tokens

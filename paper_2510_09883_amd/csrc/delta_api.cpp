@@ -385,6 +385,15 @@ int delta_workspace_bytes(const delta_shape_t* shape, const delta_select_t* sel,
   return DELTA_OK;
 }
 
+int delta_delta_path(const delta_shape_t* shape, const delta_select_t* sel, int* fused) {
+  if (!fused || !sel) return DELTA_ERR_INVALID_ARG;
+  Layout L;
+  int rc = make_layout(shape, sel, &L);
+  if (rc) return rc;
+  *fused = use_fused_delta(shape, sel, L) ? 1 : 0;
+  return DELTA_OK;
+}
+
 int delta_workspace_init(void* ws, size_t ws_bytes, void* stream) {
   if (!ws && ws_bytes) return DELTA_ERR_INVALID_ARG;
   return hip_rc(launch_fill_zero(ws, ws_bytes, static_cast<hipStream_t>(stream)));

@@ -25,7 +25,8 @@ DELTA_AGG_MAX, DELTA_AGG_SUM = 0, 1
 
 EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
             "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
-            "delta_kv_append", "delta_decode_step_hooked", "delta_status_string"]
+            "delta_kv_append", "delta_decode_step_hooked", "delta_delta_path",
+            "delta_status_string"]
 
 
 class delta_shape_t(ctypes.Structure):
@@ -172,6 +173,15 @@ def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
     kv = delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr())
     kv._tensors = (k_cache, v_cache, page_table, seq_lens)   # checked against the shape per call
     return kv
+
+
+def delta_delta_path(shape: delta_shape_t, sel: delta_select_t) -> bool:
+    """Whether delta_delta_attn_select runs the fused kernel for this shape and selection under
+    the current environment (DELTA_DELTA_PATH) and device."""
+    f = ctypes.c_int(0)
+    _check("delta_delta_path", _lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(sel),
+                                                     ctypes.byref(f)))
+    return bool(f.value)
 
 
 def delta_workspace_bytes(shape: delta_shape_t, sel: delta_select_t | None = None) -> int:

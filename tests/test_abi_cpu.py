@@ -24,7 +24,7 @@ def declared_functions(path=HEADER):
 
 def test_library_exports_every_declared_symbol(D):
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 10
     lib = ctypes.CDLL(D.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -190,3 +190,17 @@ def test_binding_refuses_host_and_mistyped_buffers(D):
         D._dev("q", q, torch.float32)
     with pytest.raises(ValueError):
         D._check_sel(s, sel, torch.zeros((1, 3), dtype=torch.int32), torch.zeros((1,), dtype=torch.int32))
+
+
+def test_delta_path_query(D, monkeypatch):
+    """Without DELTA_DELTA_PATH=fused the split path is reported; bad arguments are refused."""
+    monkeypatch.delenv("DELTA_DELTA_PATH", raising=False)
+    shape = D.make_shape(8, 28, 4, 128, 2048, 32768)
+    sel = D.make_select(2048, 128, 16, 0)
+    assert D.delta_delta_path(shape, sel) is False
+    f = ctypes.c_int(7)
+    assert D._lib.delta_delta_path(ctypes.byref(shape), None, ctypes.byref(f)) == D.DELTA_ERR_INVALID_ARG
+    assert D._lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(sel), None) == D.DELTA_ERR_INVALID_ARG
+    bad = D.make_select(2048, 4096, 16, 0)   # recency window not below the budget
+    assert D._lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(bad), ctypes.byref(f)) == D.DELTA_ERR_INVALID_ARG
+    assert f.value == 7
