@@ -140,7 +140,7 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  * per layer for 8 sequences of 32K tokens with 28 query and 4 KV heads; its `out` agrees with
  * delta_full_attn's up to summation order, not bit for bit).  Its workgroups wait
  * for the rest of their sequence for at most DELTA_FUSED_SPIN_TICKS ticks of the 100 MHz clock
- * (default 10 ms) and then hand their part to the sequence's last workgroup, so it never
+ * (default 1 ms) and then hand their part to the sequence's last workgroup, so it never
  * hangs when not all of them are resident, and gives the same results either way. */
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,

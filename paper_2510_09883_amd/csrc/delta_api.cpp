@@ -284,13 +284,15 @@ bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const La
   return grid <= cap;
 }
 
-// Longest wait of a fused-kernel workgroup at its sequence barrier: 10 ms of the 100 MHz
-// real-time clock (a resident sequence's workgroups arrive within tens of microseconds of each
-// other).  DELTA_FUSED_SPIN_TICKS overrides it (0: no wait, which forces the fallback of every
-// workgroup but the last to arrive; for tests).
+// Longest wait of a fused-kernel workgroup at its sequence barrier: 1 ms of the 100 MHz
+// real-time clock.  A resident sequence's workgroups arrive within tens of microseconds of each
+// other, and one that is not resident starts at least an attention phase (~80 us at 32K) late,
+// so 1 ms tells the two apart with a wide margin while bounding the stall of a launch that
+// shares the device.  DELTA_FUSED_SPIN_TICKS overrides it (0: no wait, which forces the
+// fallback of every workgroup but the last to arrive; for tests).
 int64_t fused_spin_ticks() {
   const char* e = getenv("DELTA_FUSED_SPIN_TICKS");
-  return e ? std::max<int64_t>(0, atoll(e)) : (int64_t)1000000;
+  return e ? std::max<int64_t>(0, atoll(e)) : (int64_t)100000;
 }
 
 int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
