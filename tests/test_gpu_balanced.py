@@ -111,3 +111,34 @@ def test_balanced_batch_limit(B):
     res = run_step(inp)
     check_step(inp, res, seqs=[0, 31, B - 2, B - 1]).assert_ok()
     _delta_equals_full(w, inp)
+
+
+def test_balanced_launch_in_graph_replays():
+    """A balanced full launch captured in a HIP graph and replayed three times, with eager
+    launches of the same call between the replays, gives the eager output bit for bit each
+    time (the arrival counters re-arm inside the captured kernel)."""
+    w, inp = _ragged(5, [4000, 2500, 3300, 1800, 4096, 2100])
+    d = D()
+    shape = shape_of(inp)
+    ws = d.alloc_workspace(shape)
+    kv = d.make_kv(inp.k_cache[0], inp.v_cache[0], inp.page_table, inp.seq_lens)
+    eager = torch.empty_like(inp.q[0])
+    d.delta_full_attn(shape, kv, inp.q[0], eager, ws)
+    torch.cuda.synchronize()
+    out = torch.full_like(inp.q[0], float("nan"))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        d.delta_full_attn(shape, kv, inp.q[0], out, ws)
+    for rep in range(3):
+        out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), rep
+        again = torch.empty_like(eager)
+        d.delta_full_attn(shape, kv, inp.q[0], again, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(again.view(torch.int16), eager.view(torch.int16)), rep
