@@ -934,7 +934,10 @@ def main():
                                            for k in layer_us},
         "delta_select_overhead": None if overhead is None else round(overhead, 4),
         "delta_fused_opt_in": None if fused_us is None else {
-            "note": "Delta layer on the opt-in fused kernel (DELTA_DELTA_PATH=fused); the step above uses the default path",
+            "note": ("Delta layer on the opt-in fused kernel (DELTA_DELTA_PATH=fused), which applies "
+                     "to this shape; the step above uses the default path. One fused workgroup per "
+                     "64-page chunk and sequence: it pays off only when that grid fills the device"),
+            "grid_workgroups": w.batch * math.ceil(math.ceil(max(lens) / 16) / 64),
             "layer_us": round(fused_us, 2),
             "delta_select_overhead": round((fused_us - layer_us["full"]) / layer_us["full"], 4)},
         "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1),
