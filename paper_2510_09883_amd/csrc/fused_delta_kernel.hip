@@ -9,8 +9,10 @@
 //   1. each wave stores its chunk partial (max, sum, o) per query head (device-coherent);
 //   2. the workgroups of a sequence wait for each other (device-scope counter), for at most
 //      a.spin_ticks of the 100 MHz real-time clock;
-//   3. every workgroup forms the log-sum-exp of all query heads from the chunk partials;
-//   4. workgroup c merges the outputs of heads c, c + n_chunks, ... in chunk order;
+//   3. every workgroup forms the log-sum-exp of all query heads from the chunk partials (one
+//      round trip for all of them);
+//   4. workgroup c merges the outputs of heads c, c + n_active, ... in chunk order (n_active:
+//      the chunks the sequence has), its loads in flight while it scores;
 //   5. every workgroup scores its own tokens from its LDS logits, s_t = 2^(max_j (x_j(t) -
 //      lse_j)) (or sum_j 2^(x_j(t) - lse_j)), sums them per page and stores the page scores;
 //   6. the last workgroup of the sequence to finish scoring selects for it (select_impl.h).
