@@ -14,7 +14,7 @@
 // (full / Delta layers) over a ragged batch of 2-64 sequences instead cuts the batch's actual
 // groups, in (b, g, page) order, into equal runs, one per workgroup, each run possibly
 // spanning pairs, so that every CU gets the same work whatever the spread of sequence
-// lengths; with equal lengths the two cuts coincide.  Waves take a piece's groups in interleaved blocks of four and keep their
+// lengths; with equal or nearly equal lengths the static cut is kept.  Waves take a piece's groups in interleaved blocks of four and keep their
 // own online-softmax state; all G query heads of the KV group share every K/V byte read.
 //
 // Per group and wave:
@@ -371,8 +371,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     // run may span pairs; a pair is combined from the pieces the run boundaries cut it into,
     // in order.  An empty sequence counts as one group (its piece writes the empty output).
     // Every wave derives the same cut from the sequence lengths (one per lane: B <= 64), and it
-    // is taken only when no run spans more than three pairs (chunk <= 2 x the shortest pair);
-    // with equal lengths the runs are exactly the static pieces.
+    // is taken only when no run spans more than three pairs (chunk <= 2 x the shortest pair)
+    // and when it pays (below).
     const int B = gridDim.z;
     if (lane < B) {
       bal_len = a.seq_lens[lane];
@@ -387,7 +387,12 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     const int W = Hkv * total;
     const int n_wg = gridDim.x * gridDim.y * gridDim.z;
     const int chunk = max((W + n_wg - 1) / n_wg, a.chunk_min);
-    if (chunk <= 2 * shortest) {   // uniform over the launch
+    // Taken only when it shortens the longest run by a tenth or more against the static
+    // pieces (gps groups); equal or nearly equal lengths keep the static split, whose pieces
+    // never straddle a pair.  Otherwise, with lengths that are not a multiple of the run, the
+    // run boundaries drift through successive pairs and leave slivers of a few groups, each
+    // with a piece's fixed costs.
+    if (chunk <= 2 * shortest && 10 * chunk <= 9 * a.gps) {   // uniform over the launch
       bal_chunk = chunk;
       bal_w = split + gridDim.x * (g_s + Hkv * b_s);
       bal_x = bal_w * chunk;
