@@ -90,14 +90,16 @@ typedef struct {
   const int32_t* seq_lens;    /* int32 [batch]: tokens cached, the current one included       */
 } delta_kv_t;
 
-/* Selection parameters (Sec. 4; App. A, Alg. 2).  All counts are in TOKENS and must be whole
- * units: budget k = K*U, recency window l = L*U.  unit_tokens U = 16 is page-based DELTA (the
- * paper's configuration); U = 1 is the token-level rule of Sec. 4.  A sequence may have at most
- * 8192 candidate units (units older than the recency window): 131072 tokens with pages, about
- * 8192 with single tokens; larger shapes return DELTA_ERR_UNSUPPORTED. */
+/* Selection parameters (Sec. 4; App. A, Alg. 2).  All counts are in TOKENS.  The budget must
+ * be whole units: k = K*U.  The recency window may be any token count l >= 0: it keeps the last
+ * L = ceil(l / U) units (App. A, Alg. 1 rounds the window up to whole pages), and L < K is
+ * required.  unit_tokens U = 16 is page-based DELTA (the paper's configuration); U = 1 is the
+ * token-level rule of Sec. 4.  A sequence may have at most 8192 candidate units (units older
+ * than the recency window): 131072 tokens with pages, about 8192 with single tokens; larger
+ * shapes return DELTA_ERR_UNSUPPORTED. */
 typedef struct {
   int32_t budget_tokens;      /* k: tokens kept per sequence, a multiple of U, > recent       */
-  int32_t recent_tokens;      /* l: most recent tokens always kept, a multiple of U, >= 0     */
+  int32_t recent_tokens;      /* l: most recent tokens always kept (ceil(l/U) units), >= 0   */
   int32_t unit_tokens;        /* U: 16 (pages) or 1 (tokens)                                  */
   int32_t agg;                /* DELTA_AGG_MAX (paper) or DELTA_AGG_SUM                       */
 } delta_select_t;

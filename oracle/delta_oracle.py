@@ -176,6 +176,15 @@ def unit_scores(s_tok: np.ndarray, unit_tokens: int) -> np.ndarray:
     return S
 
 
+def recent_units_of(recent_tokens: int, unit_tokens: int) -> int:
+    """The recency window in units: App. A, Alg. 1 keeps the last ceil(L / P) pages for a
+    window of L tokens, so any token count is a valid window; with units of U tokens it is the
+    last ceil(l / U) units."""
+    if recent_tokens < 0 or unit_tokens < 1:
+        raise ValueError("need l >= 0 and U >= 1")
+    return -(-recent_tokens // unit_tokens)
+
+
 def select_units(S: np.ndarray, budget_units: int, recent_units: int) -> np.ndarray:
     """rho = last L units  U  top-(K - L) of the older units by S (Sec. 4; Alg. 2).
 

@@ -144,14 +144,23 @@ int check_shape(const delta_shape_t* s) {
   return DELTA_OK;
 }
 
+// The recency window in units.  App. A, Alg. 1 keeps the last ceil(L / P) pages for a window
+// of L tokens, so any token count is valid: the window is the last ceil(l / U) units.
+int recent_units_of(const delta_select_t* sel) {
+  return ceil_div(sel->recent_tokens, sel->unit_tokens);
+}
+
 int check_select(const delta_select_t* sel) {
   if (!sel) return DELTA_ERR_INVALID_ARG;
   if (sel->unit_tokens != 16 && sel->unit_tokens != 1) return DELTA_ERR_UNSUPPORTED;
   if (sel->agg != DELTA_AGG_MAX && sel->agg != DELTA_AGG_SUM) return DELTA_ERR_INVALID_ARG;
   if (sel->budget_tokens < 1 || sel->recent_tokens < 0) return DELTA_ERR_INVALID_ARG;
-  if (sel->budget_tokens % sel->unit_tokens || sel->recent_tokens % sel->unit_tokens)
+  if (sel->budget_tokens % sel->unit_tokens) return DELTA_ERR_INVALID_ARG;
+  // L < K, counted in units (a window that rounds up to the whole budget leaves no choice);
+  // the token comparison comes first and keeps the rounding below from overflowing
+  if (sel->recent_tokens >= sel->budget_tokens ||
+      recent_units_of(sel) >= sel->budget_tokens / sel->unit_tokens)
     return DELTA_ERR_INVALID_ARG;
-  if (sel->recent_tokens >= sel->budget_tokens) return DELTA_ERR_INVALID_ARG;   // L < K
   return DELTA_OK;
 }
 
@@ -177,7 +186,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     }
     L->max_split = std::max(L->max_split, L->sparse.slots);
     // the selection holds the older units of one sequence in one workgroup's registers
-    if (ceil_div(s->max_seq_len, sel->unit_tokens) - sel->recent_tokens / sel->unit_tokens > kMaxSelectKeys)
+    if (ceil_div(s->max_seq_len, sel->unit_tokens) - recent_units_of(sel) > kMaxSelectKeys)
       return DELTA_ERR_UNSUPPORTED;
   }
   L->logit_pages = ceil_div(s->max_seq_len, 16);
@@ -264,7 +273,7 @@ bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const La
   if (!e || strcmp(e, "fused")) return false;
   const int G = s->n_q_heads / s->n_kv_heads;
   if (s->head_dim != 128 || s->n_kv_heads % 4 != 0 || s->n_q_heads > kFusedMaxQHeads) return false;
-  const int n_c = L.nu_stride - sel->recent_tokens / sel->unit_tokens;
+  const int n_c = L.nu_stride - recent_units_of(sel);
   if (n_c > kFusedKeysPerThread * 256) return false;
   if (L.fused_chunks > kFusedMaxChunks) return false;
   const int64_t grid = (int64_t)L.fused_chunks * s->batch;
@@ -309,7 +318,7 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
   xa.nu_stride = L.nu_stride;
   xa.unit_tokens = sel->unit_tokens;
   xa.budget_units = sel->budget_tokens / sel->unit_tokens;
-  xa.recent_units = sel->recent_tokens / sel->unit_tokens;
+  xa.recent_units = recent_units_of(sel);
   if (use_fused_delta(s, sel, L)) {
     FusedArgs f{};
     f.k_cache = static_cast<const uint16_t*>(kv->k_cache);

@@ -123,7 +123,7 @@ def check_step(inp, res, seqs=None, layers=None, roles=None, agg=0, budget=None,
     roles = w.roles if roles is None else roles
     U = w.unit_tokens
     K_u = (w.budget_tokens if budget is None else budget) // U
-    L_u = (w.recent_tokens if recent is None else recent) // U
+    L_u = O.recent_units_of(w.recent_tokens if recent is None else recent, U)
     seqs = range(w.batch) if seqs is None else seqs
     layers = range(len(roles)) if layers is None else sorted(layers)
     rep = report or Report()

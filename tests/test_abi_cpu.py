@@ -83,7 +83,7 @@ def test_shape_validation(D, kw, status):
     ((2048, 2048), -1),                # L >= K (only L < K is valid, App. C)
     ((2048, 4096), -1),
     ((2040, 128), -1),                 # budget not a whole number of pages
-    ((2048, 120), -1),                 # window not a whole number of pages
+    ((2048, 2033), -1),                # a window of 2033 tokens rounds up to 128 pages = K
     ((0, 0), -1),
 ])
 def test_select_validation(D, sel, status):
@@ -94,6 +94,15 @@ def test_select_validation(D, sel, status):
         D.delta_workspace_bytes(shape(D), D.make_select(2048, 128, unit_tokens=8))
     with pytest.raises(D.DeltaError):
         D.delta_workspace_bytes(shape(D), D.make_select(2048, 128, agg=2))
+
+
+@pytest.mark.parametrize("budget,recent", [(2048, 120), (2048, 8), (2048, 2032), (128, 1), (32, 15)])
+def test_recency_window_of_any_token_count(D, budget, recent):
+    """App. A, Alg. 1 keeps ceil(L / P) pages for a window of L tokens: a window that is not a
+    whole number of pages is valid as long as its rounded-up page count stays below K."""
+    assert D.delta_workspace_bytes(shape(D), D.make_select(budget, recent)) > 0
+    # token-level units take every window as is
+    assert D.delta_workspace_bytes(shape(D), D.make_select(budget, recent, unit_tokens=1)) > 0
 
 
 def test_selection_key_limit(D):

@@ -135,3 +135,19 @@ def test_random_batches_cover_every_page_once():
         _, _, balanced = check(lens, Hkv, mg, target=rng.choice([256, 512, 64]))
         seen_balanced += balanced
     assert seen_balanced > 80
+
+
+def test_gpu_test_batches_take_the_balanced_cut():
+    """Every batch of tests/test_gpu_balanced.py that is meant to run the balanced cut takes it
+    under the model above (and the batch one past the lane limit does not), so a change to the
+    cut's threshold cannot move those GPU tests onto the static split unnoticed."""
+    import balanced_cases as BC
+    for _, hkv, lens in BC.RAGGED:
+        assert check(lens, hkv, cdiv(max(lens), 16))[2], lens
+    for _, seed in BC.RANDOM:
+        hkv, _, lens = BC.random_case(seed)
+        assert check(lens, hkv, cdiv(max(lens), 16))[2], seed
+    for B in BC.BATCH_LIMIT:
+        lens = BC.batch_limit_lens(B)
+        taken = check(lens, BC.BATCH_LIMIT_KV_HEADS, cdiv(max(lens), 16))[2]
+        assert taken == (B <= BAL_MAX_BATCH), B

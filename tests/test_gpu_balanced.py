@@ -19,6 +19,7 @@ layer's, bit for bit (App. A, Alg. 1: the Delta layer's attention is the full at
 import pytest
 import torch
 
+import balanced_cases as BC
 from gpu_helpers import D, check_step, log, run_step, select_of, shape_of
 from paper_2510_09883_amd import configs, synth
 
@@ -53,8 +54,7 @@ def _delta_equals_full(w, inp, layer=1):
     assert torch.equal(out_f.view(torch.int16), out_d.view(torch.int16))
 
 
-@pytest.mark.parametrize("cid,lens", [(5, [4000, 2500, 3300, 1800, 4096, 2100]),
-                                      (4, [76, 1379, 1267, 696, 1455, 170, 174, 86, 65, 157, 168, 827])])
+@pytest.mark.parametrize("cid,lens", [(c, lens) for c, _, lens in BC.RAGGED])
 def test_balanced_runs_match_oracle(cid, lens):
     w, inp = _ragged(cid, lens)
     d = D()
@@ -70,23 +70,17 @@ def test_balanced_runs_match_oracle(cid, lens):
 
 
 def _random_case(seed, G):
-    """A seeded random shape with group size G (2, 4 or 8 KV heads, head dim 64 or 128, 6-24
-    sequences of lengths in [L/4, L]; shuffled page tables on odd seeds).  The seeds are ones
-    whose batch takes the balanced cut (the CPU model of tests/test_balanced_cut.py says so)."""
-    import random
-    r = random.Random(seed)
-    hkv = r.choice([2, 4, 8])
-    d = r.choice([64, 128])
-    B = r.randint(6, 24)
-    L = r.randint(600, 3000)
-    lens = [r.randint(L // 4, L) for _ in range(B)]
-    w = configs.Workload(90 + seed, f"random{seed}", 3, G * hkv, hkv, d, B, max(lens), 256,
+    """A seeded random shape with group size G (tests/balanced_cases.py; shuffled page tables
+    on odd seeds).  The seeds are ones whose batch takes the balanced cut, which
+    tests/test_balanced_cut.py checks on the CPU model of the cut."""
+    hkv, d, lens = BC.random_case(seed)
+    w = configs.Workload(90 + seed, f"random{seed}", 3, G * hkv, hkv, d, len(lens), max(lens), 256,
                          hh_frac=0.02, shuffled_pages=bool(seed % 2),
                          roles=[configs.ROLE_FULL, configs.ROLE_DELTA, configs.ROLE_SPARSE])
     return w, lens
 
 
-@pytest.mark.parametrize("G,seed", [(1, 0), (2, 9), (3, 10), (4, 3), (5, 4), (6, 5), (7, 6), (8, 7)])
+@pytest.mark.parametrize("G,seed", BC.RANDOM)
 def test_balanced_random_shapes(G, seed):
     w, lens = _random_case(seed, G)
     log(f"random case {seed}: Hq {w.n_q_heads} Hkv {w.n_kv_heads} d {w.head_dim} lens {lens}")
@@ -97,13 +91,11 @@ def test_balanced_random_shapes(G, seed):
     _delta_equals_full(w, inp)
 
 
-@pytest.mark.parametrize("B", [64, 65])
+@pytest.mark.parametrize("B", BC.BATCH_LIMIT)
 def test_balanced_batch_limit(B):
     """64 sequences fill the lanes of the balanced cut; at 65 the host keeps the static split.
     Qwen-1.5B attention shape (12/2/128) with lengths in [400, 800]."""
-    import random
-    r = random.Random(B)
-    lens = [r.randint(400, 800) for _ in range(B)]
+    lens = BC.batch_limit_lens(B)
     w = configs.get(6)
     w.batch = B
     w.n_layers = 3
@@ -120,7 +112,8 @@ def test_balanced_launch_in_graph_replays():
     """A balanced full launch captured in a HIP graph and replayed three times, with eager
     launches of the same call between the replays, gives the eager output bit for bit each
     time (the arrival counters re-arm inside the captured kernel)."""
-    w, inp = _ragged(5, [4000, 2500, 3300, 1800, 4096, 2100])
+    cid, _, lens = BC.RAGGED[0]
+    w, inp = _ragged(cid, lens)
     d = D()
     shape = shape_of(inp)
     ws = d.alloc_workspace(shape)

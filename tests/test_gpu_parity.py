@@ -119,11 +119,14 @@ def test_physical_selection_matches_page_table(U):
 # ------------------------------------------------------------------------------------------
 # Config 2 (Llama-8B shape, B=1, 8k): every layer of the step
 # ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("agg", [0, 1])
 @pytest.mark.parametrize("U", [16, 1])
-def test_config2_step(U):
+def test_config2_step(U, agg):
+    """32 query heads: the scoring kernel's eight-head load batches, for the paper's maximum
+    over heads and for the sum (Sec. 4 "Selection mechanism"; App. A, Alg. 2)."""
     inp = _inputs(2, U)
-    res = run_step(inp)
-    check_step(inp, res).assert_ok()
+    res = run_step(inp, agg=agg)
+    check_step(inp, res, agg=agg).assert_ok()
 
 
 # ------------------------------------------------------------------------------------------
@@ -139,8 +142,10 @@ def test_ragged_and_short_lengths(lens):
     check_step(inp, res).assert_ok()
 
 
-@pytest.mark.parametrize("recent", [0, 16, 112])
+@pytest.mark.parametrize("recent", [0, 16, 112, 8, 17, 100])
 def test_recency_window_sizes(recent):
+    """Windows of whole pages and of token counts that round up to the next page (App. A,
+    Alg. 1: ceil(L / P) pages)."""
     inp = _inputs(1)
     res = run_step(inp, recent=recent)
     check_step(inp, res, recent=recent).assert_ok()
@@ -255,15 +260,15 @@ def test_graph_replay_matches_eager():
 # ------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("cfg,seqs", [(3, [0, 9]), (4, [0, 5]), (5, [0, 17, 31]), (6, [0, 63]),
                                       (7, [1, 40]), (8, [0, 31])])
-def test_full_size_sampled(cfg, seqs):
+def test_full_size_sampled(cfg, seqs, agg=0):
     inp = _inputs(cfg)
     w = inp.workload
-    res = run_step(inp)
+    res = run_step(inp, agg=agg)
     log("device step done; checking sampled sequences")
     first_sparse = [i for i, r in enumerate(w.roles) if r == ROLE_SPARSE]
     deltas = [i for i, r in enumerate(w.roles) if r == ROLE_DELTA]
     layers = sorted({0, 1, *deltas, first_sparse[0], first_sparse[-1]})
-    rep = check_step(inp, res, seqs=seqs, layers=layers, use_page_table=False)
+    rep = check_step(inp, res, seqs=seqs, layers=layers, use_page_table=False, agg=agg)
     rep.assert_ok()
     # every sequence's selection is structurally valid (size, order, recency units)
     cnt = res.sel_cnt.cpu().numpy()
@@ -278,6 +283,13 @@ def test_full_size_sampled(cfg, seqs):
             assert set(range(n_u - w.recent_units, n_u)) <= set(r.tolist())
     del inp, res
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cfg,seqs", [(4, [0, 7]), (5, [0, 31])])
+def test_full_size_sampled_sum_aggregation(cfg, seqs):
+    """The sum over heads at the full-size head counts: 28 query heads (the last load batch of
+    every scoring wave is part masked) and 32 (Sec. 4 "Selection mechanism" reading)."""
+    test_full_size_sampled(cfg, seqs, agg=1)
 
 
 def test_shared_workspace_alternating_inputs():

@@ -271,6 +271,23 @@ def test_selection_invariants_and_nesting():
             prev = r
 
 
+def test_recency_window_in_units_brute_force():
+    """Alg. 1 keeps ceil(L / P) pages for a window of L tokens.  Pinned by brute force: for a
+    context of whole units, the units the window keeps are exactly the units that hold any of
+    the last l tokens (a floor or a rounding would drop the unit of the window's oldest
+    tokens, or keep a unit too many)."""
+    for U in (1, 4, 16):
+        for n_u in (1, 2, 3, 9):
+            s = n_u * U
+            for l in range(0, s + 1):
+                touched = {t // U for t in range(s - l, s)}
+                L_u = O.recent_units_of(l, U)
+                assert set(range(n_u - L_u, n_u)) == touched, (U, n_u, l)
+    assert O.recent_units_of(0, 16) == 0 and O.recent_units_of(8, 16) == 1
+    with pytest.raises(ValueError):
+        O.recent_units_of(-1, 16)
+
+
 def test_token_level_topk_of_raw_logits():
     # one head, U = 1, L = 0: softmax is monotone, so rho is the top-k of the raw logits
     rng = _rng(7)
