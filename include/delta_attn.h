@@ -221,6 +221,27 @@ int delta_decode_step_hooked(const delta_shape_t* shape, int32_t n_layers, const
                              const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
                              void* ws, size_t ws_bytes, void* stream, const delta_hooks_t* hooks);
 
+/* Largest workspace the allocation-free step below can serve: the library's scratch array, one
+ * per GPU, held from the first delta_decode_step_noalloc call on that GPU until the process
+ * ends.  160 MiB covers a 32-layer step of 32 sequences of up to 32K tokens with 32 query and
+ * 8 KV heads (delta_workspace_bytes: 145 MiB). */
+#define DELTA_NOALLOC_SCRATCH_BYTES ((size_t)160 << 20)
+
+/* delta_decode_step for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the same arguments and results
+ * (bit for bit) without `ws` / `ws_bytes`; the library's own scratch array takes the
+ * workspace's place.  It calls no hipMalloc, hipFree or other allocating routine (the first call
+ * on a GPU looks up the array's address there, which loads it).  Each call first clears the
+ * arrival counters in the scratch with a small kernel, then enqueues the step, so any sequence of
+ * shapes may follow any other.  All calls on one GPU share its array: calls that may overlap on
+ * one GPU (other streams, other threads) race and must be serialised by the caller.
+ * Returns DELTA_ERR_WORKSPACE, before any device call, when delta_workspace_bytes() for this
+ * shape and selection exceeds DELTA_NOALLOC_SCRATCH_BYTES; other errors as delta_decode_step. */
+int delta_decode_step_noalloc(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                              const delta_kv_t* kv, const void* const* q, void* const* out,
+                              const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
+                              void* stream);
+
 /* Static description of a status code. */
 const char* delta_status_string(int status);
 

@@ -16,7 +16,7 @@ LIB = os.path.join(PKG, "libdelta_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["attn_kernel.hip", "fused_delta_kernel.hip", "select_kernel.hip", "append_kernel.hip",
-           "probe_kernel.hip", "delta_api.cpp"]
+           "probe_kernel.hip", "noalloc.hip", "delta_api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-mcode-object-version=5",
     # no packed fp32 VALU instructions: scalar/float2 code is compiled to unpacked ops

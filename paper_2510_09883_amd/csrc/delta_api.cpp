@@ -18,6 +18,8 @@ namespace {
 
 using namespace delta;
 
+static_assert(kNoallocScratchBytes == DELTA_NOALLOC_SCRATCH_BYTES, "scratch size of the C ABI");
+
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -381,6 +383,65 @@ int run_sparse(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void
                                  s->batch, st));
 }
 
+// Argument checks of a decoding step (every layer's buffers, roles and selection slots) and
+// its workspace layout.  Nothing is enqueued.
+int check_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+               const delta_kv_t* kv, const void* const* q, void* const* out,
+               const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, Layout* L) {
+  if (n_layers < 0 || (n_layers > 0 && (!roles || !kv || !q || !out))) return DELTA_ERR_INVALID_ARG;
+  int n_delta = 0, n_sel_users = 0;
+  for (int i = 0; i < n_layers; ++i) {
+    if (roles[i] < DELTA_ROLE_FULL || roles[i] > DELTA_ROLE_SPARSE) return DELTA_ERR_INVALID_ARG;
+    n_delta += roles[i] == DELTA_ROLE_DELTA;
+    n_sel_users += roles[i] != DELTA_ROLE_FULL;
+  }
+  if (n_sel_users && !sel) return DELTA_ERR_INVALID_ARG;
+  if (n_delta && (!sel_idx || !sel_cnt)) return DELTA_ERR_INVALID_ARG;
+  int rc = make_layout(shape, n_sel_users ? sel : nullptr, L);
+  if (rc) return rc;
+  for (int i = 0; i < n_layers; ++i) {
+    if ((rc = check_kv(&kv[i]))) return rc;
+    if (!q[i] || !out[i]) return DELTA_ERR_INVALID_ARG;
+  }
+  return DELTA_OK;
+}
+
+// The layer loop of App. A, Alg. 1 over a checked step, on workspace `w` laid out as `L`.
+int enqueue_step(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                 const delta_kv_t* kv, const void* const* q, void* const* out,
+                 const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, const Layout& L,
+                 char* w, void* stream, const delta_hooks_t* hooks) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int K = sel ? sel->budget_tokens / sel->unit_tokens : 0;
+  const size_t slot = (size_t)shape->batch * K;
+  int cur = -1;   // most recent Delta slot; -1 = every unit (App. A, Alg. 1 initialisation)
+  // Each Delta layer also leaves the physical locations of its selection in the workspace,
+  // read through its page table; later sparse layers that share that page table use them.
+  int32_t* phys = sel ? reinterpret_cast<int32_t*>(w + L.phys) : nullptr;
+  const int32_t* phys_pt = nullptr;
+  int rc = DELTA_OK;
+  for (int i = 0; i < n_layers; ++i) {
+    if (hooks && hooks->before_attn && hooks->before_attn(i, hooks->user, stream))
+      return DELTA_ERR_HOOK;
+    if (roles[i] == DELTA_ROLE_FULL || (roles[i] == DELTA_ROLE_SPARSE && cur < 0)) {
+      rc = run_full(shape, &kv[i], q[i], out[i], L, w, st);
+    } else if (roles[i] == DELTA_ROLE_DELTA) {
+      ++cur;
+      rc = run_delta(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
+                     sel_cnt + (size_t)cur * shape->batch, nullptr, phys, L, w, st);
+      phys_pt = kv[i].page_table;
+    } else {
+      rc = run_sparse(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
+                      sel_cnt + (size_t)cur * shape->batch,
+                      kv[i].page_table == phys_pt ? phys : nullptr, L, w, st);
+    }
+    if (rc) return rc;
+    if (hooks && hooks->after_attn && hooks->after_attn(i, hooks->user, stream))
+      return DELTA_ERR_HOOK;
+  }
+  return DELTA_OK;
+}
+
 }  // namespace
 
 // Only the C ABI is exported; everything else in the library has hidden visibility.
@@ -485,53 +546,36 @@ int delta_decode_step_hooked(const delta_shape_t* shape, int32_t n_layers, const
                              const delta_kv_t* kv, const void* const* q, void* const* out,
                              const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
                              void* ws, size_t ws_bytes, void* stream, const delta_hooks_t* hooks) {
-  if (n_layers < 0 || (n_layers > 0 && (!roles || !kv || !q || !out)) || !ws)
-    return DELTA_ERR_INVALID_ARG;
-  int n_delta = 0, n_sel_users = 0;
-  for (int i = 0; i < n_layers; ++i) {
-    if (roles[i] < DELTA_ROLE_FULL || roles[i] > DELTA_ROLE_SPARSE) return DELTA_ERR_INVALID_ARG;
-    n_delta += roles[i] == DELTA_ROLE_DELTA;
-    n_sel_users += roles[i] != DELTA_ROLE_FULL;
-  }
-  if (n_sel_users && !sel) return DELTA_ERR_INVALID_ARG;
-  if (n_delta && (!sel_idx || !sel_cnt)) return DELTA_ERR_INVALID_ARG;
+  if (!ws) return DELTA_ERR_INVALID_ARG;
   Layout L;
-  int rc = make_layout(shape, n_sel_users ? sel : nullptr, &L);
+  int rc = check_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, &L);
   if (rc) return rc;
   if (ws_bytes < L.total) return DELTA_ERR_WORKSPACE;
-  for (int i = 0; i < n_layers; ++i) {
-    if ((rc = check_kv(&kv[i]))) return rc;
-    if (!q[i] || !out[i]) return DELTA_ERR_INVALID_ARG;
-  }
+  return enqueue_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, L,
+                      static_cast<char*>(ws), stream, hooks);
+}
+
+int delta_decode_step_noalloc(const delta_shape_t* shape, int32_t n_layers, const int32_t* roles,
+                              const delta_kv_t* kv, const void* const* q, void* const* out,
+                              const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
+                              void* stream) {
+  Layout L;
+  int rc = check_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, &L);
+  if (rc) return rc;
+  if (L.total > kNoallocScratchBytes) return DELTA_ERR_WORKSPACE;   // before any device call
+  void* ws = nullptr;
+  if (noalloc_scratch(&ws) != hipSuccess) return DELTA_ERR_HIP;
   char* w = static_cast<char*>(ws);
+  // The scratch keeps whatever the previous call on this device left, laid out for that call's
+  // shape; the arrival counters of this call's layout must start at zero (every other region is
+  // written before it is read, and the kernels re-arm the counters they use).
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int K = sel ? sel->budget_tokens / sel->unit_tokens : 0;
-  const size_t slot = (size_t)shape->batch * K;
-  int cur = -1;   // most recent Delta slot; -1 = every unit (App. A, Alg. 1 initialisation)
-  // Each Delta layer also leaves the physical locations of its selection in the workspace,
-  // read through its page table; later sparse layers that share that page table use them.
-  int32_t* phys = sel ? reinterpret_cast<int32_t*>(w + L.phys) : nullptr;
-  const int32_t* phys_pt = nullptr;
-  for (int i = 0; i < n_layers; ++i) {
-    if (hooks && hooks->before_attn && hooks->before_attn(i, hooks->user, stream))
-      return DELTA_ERR_HOOK;
-    if (roles[i] == DELTA_ROLE_FULL || (roles[i] == DELTA_ROLE_SPARSE && cur < 0)) {
-      rc = run_full(shape, &kv[i], q[i], out[i], L, w, st);
-    } else if (roles[i] == DELTA_ROLE_DELTA) {
-      ++cur;
-      rc = run_delta(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
-                     sel_cnt + (size_t)cur * shape->batch, nullptr, phys, L, w, st);
-      phys_pt = kv[i].page_table;
-    } else {
-      rc = run_sparse(shape, &kv[i], q[i], out[i], sel, sel_idx + cur * slot,
-                      sel_cnt + (size_t)cur * shape->batch,
-                      kv[i].page_table == phys_pt ? phys : nullptr, L, w, st);
-    }
-    if (rc) return rc;
-    if (hooks && hooks->after_attn && hooks->after_attn(i, hooks->user, stream))
-      return DELTA_ERR_HOOK;
-  }
-  return DELTA_OK;
+  const size_t pairs = (size_t)shape->batch * shape->n_kv_heads;
+  const size_t fused_bytes = L.fcnt ? L.total - L.fcnt : 0;   // fused counters and chunk flags
+  if (launch_fill_zero2(w + L.counters, sizeof(int32_t) * pairs, w + L.fcnt, fused_bytes, st) != hipSuccess)
+    return DELTA_ERR_HIP;
+  return enqueue_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, L, w, stream,
+                      nullptr);
 }
 
 const char* delta_status_string(int status) {

@@ -124,5 +124,12 @@ struct AppendArgs {
 hipError_t launch_kv_append(const AppendArgs& a, int batch, hipStream_t stream);
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+hipError_t launch_fill_zero2(void* p0, size_t bytes0, void* p1, size_t bytes1, hipStream_t stream);
+
+// Library-held scratch of the allocation-free decode step: one array of this many bytes per
+// GPU (DELTA_NOALLOC_SCRATCH_BYTES of the C ABI), allocated when the step first runs there.
+// *ptr gets the current device's copy.
+constexpr size_t kNoallocScratchBytes = (size_t)160 << 20;
+hipError_t noalloc_scratch(void** ptr);
 
 }  // namespace delta

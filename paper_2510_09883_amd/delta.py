@@ -26,7 +26,8 @@ DELTA_AGG_MAX, DELTA_AGG_SUM = 0, 1
 EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
             "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
             "delta_kv_append", "delta_decode_step_hooked", "delta_delta_path",
-            "delta_status_string"]
+            "delta_decode_step_noalloc", "delta_status_string"]
+DELTA_NOALLOC_SCRATCH_BYTES = 160 << 20
 
 
 class delta_shape_t(ctypes.Structure):
@@ -75,6 +76,9 @@ def _bind(lib):
     lib.delta_decode_step_hooked.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
                                              _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
                                              _vp, _vp, _vp, ctypes.c_size_t, _vp, _P(delta_hooks_t)]
+    lib.delta_decode_step_noalloc.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
+                                              _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
+                                              _vp, _vp, _vp]
     lib.delta_hbm_read_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, ctypes.c_int32, _vp]
     lib.delta_hbm_read_probe.restype = ctypes.c_int
     lib.delta_status_string.argtypes = [ctypes.c_int]
@@ -259,7 +263,8 @@ class StepArgs:
             _dev("sel_cnt", sel_cnt, torch.int32, (None, shape.batch))
             if sel_idx.shape[0] < n_delta or sel_cnt.shape[0] < n_delta:
                 raise ValueError(f"sel_idx / sel_cnt need a slot for each of the {n_delta} Delta layers")
-        _dev("ws", ws)
+        if ws is not None:   # None: only for delta_decode_step_noalloc
+            _dev("ws", ws)
         self.shape = shape
         self.n = n
         self.roles = (ctypes.c_int32 * n)(*roles)
@@ -278,6 +283,15 @@ def delta_decode_step(args: StepArgs):
                                   ctypes.byref(a.sel) if a.sel is not None else None,
                                   _ptr(a.sel_idx), _ptr(a.sel_cnt), _ptr(a.ws), _nbytes(a.ws),
                                   _stream()))
+
+
+def delta_decode_step_noalloc(args: StepArgs):
+    """delta_decode_step on the library's own scratch memory (args.ws is not used)."""
+    a = args
+    _check("delta_decode_step_noalloc",
+           _lib.delta_decode_step_noalloc(ctypes.byref(a.shape), a.n, a.roles, a.kvs, a.qs, a.outs,
+                                          ctypes.byref(a.sel) if a.sel is not None else None,
+                                          _ptr(a.sel_idx), _ptr(a.sel_cnt), _stream()))
 
 
 def delta_kv_append(shape, k_cache, v_cache, page_table, seq_lens, k_new, v_new):

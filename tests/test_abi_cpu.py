@@ -24,7 +24,7 @@ def declared_functions(path=HEADER):
 
 def test_library_exports_every_declared_symbol(D):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     lib = ctypes.CDLL(D.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -144,6 +144,30 @@ def test_calls_reject_before_launch(D):
     assert lib.delta_decode_step(P(s), 3, roles_bad, kvs, ptrs, ptrs, P(sel), fake, fake, fake, need, None) == -1
     nullq = (ctypes.c_void_p * 3)(0x1000, None, 0x1000)
     assert lib.delta_decode_step(P(s), 3, roles, kvs, nullq, ptrs, P(sel), fake, fake, fake, need, None) == -1
+
+
+def test_noalloc_step_rejects_before_any_device_call(D):
+    """The allocation-free step checks its arguments and its scratch size on the host: a shape
+    whose workspace exceeds the library's scratch returns DELTA_ERR_WORKSPACE (not a HIP error:
+    there is no GPU here), and bad arguments DELTA_ERR_INVALID_ARG."""
+    lib = D._lib
+    P = ctypes.byref
+    fake = ctypes.c_void_p(0x1000)
+    kv = D.delta_kv_t(1, 2, 3, 4)
+    kvs = (D.delta_kv_t * 3)(kv, kv, kv)
+    ptrs = (ctypes.c_void_p * 3)(0x1000, 0x1000, 0x1000)
+    roles = (ctypes.c_int32 * 3)(0, 1, 2)
+    sel = D.make_select(2048, 128)
+    big = D.make_shape(64, 32, 8, 128, 2048, 32768)
+    assert D.delta_workspace_bytes(big, sel) > D.DELTA_NOALLOC_SCRATCH_BYTES
+    assert lib.delta_decode_step_noalloc(P(big), 3, roles, kvs, ptrs, ptrs, P(sel), fake, fake, None) == -3
+    s = shape(D)
+    assert D.delta_workspace_bytes(s, sel) <= D.DELTA_NOALLOC_SCRATCH_BYTES
+    assert lib.delta_decode_step_noalloc(P(s), 3, roles, kvs, ptrs, ptrs, None, fake, fake, None) == -1
+    assert lib.delta_decode_step_noalloc(P(s), 3, roles, kvs, ptrs, ptrs, P(sel), None, fake, None) == -1
+    bad_roles = (ctypes.c_int32 * 3)(0, 5, 2)
+    assert lib.delta_decode_step_noalloc(P(s), 3, bad_roles, kvs, ptrs, ptrs, P(sel), fake, fake, None) == -1
+    assert lib.delta_decode_step_noalloc(P(s), -1, roles, kvs, ptrs, ptrs, P(sel), fake, fake, None) == -1
 
 
 def test_append_and_hooked_step_reject_before_launch(D):
