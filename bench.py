@@ -178,7 +178,7 @@ def read_ceiling(D):
             "kernel": "delta_hbm_read_probe (16-byte streaming loads)"}
 
 
-def time_layers(D, w, sets, stack, shape, sel, ws, steps, fused=False):
+def time_layers(D, w, sets, stack, shape, sel, ws, steps, other_sel=None):
     """Average duration of one launch of each role's entry point.  For each role, every layer
     of the stack runs that role (its own K/V cache and query), the n launches of one step are
     captured in a HIP graph (one graph per rotating input set), and the graphs are replayed
@@ -186,9 +186,9 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps, fused=False):
     over the number of launches.  Host launch latency and per-call event overhead are excluded;
     the gap between kernels inside a graph is included.  Sparse launches use the selection of
     the Delta layer that precedes them in the schedule (the first Delta layer's for layers
-    before it), with its physical pages, as delta_decode_step does.  With `fused`, the Delta
-    role is also timed on the opt-in fused kernel ("delta_fused", captured with
-    DELTA_DELTA_PATH=fused).  Also returns how many layers of the step run each role."""
+    before it), with its physical pages, as delta_decode_step does.  With `other_sel` (the
+    selection parameters with the other Delta-layer path), the Delta role is also timed on that
+    path ("delta_other").  Also returns how many layers of the step run each role."""
     roles = stack.roles
     slots, cur = [], -1
     for r in roles:
@@ -221,21 +221,18 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps, fused=False):
         kv = D.make_kv(inp.k_cache[i], inp.v_cache[i], inp.page_table, inp.seq_lens)
         if name == "full":
             D.delta_full_attn(shape, kv, inp.q[i], out, ws)
-        elif name in ("delta", "delta_fused"):
-            D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel, scratch_idx, scratch_cnt, None,
-                                      ws, sel_phys=scratch_phys)
+        elif name in ("delta", "delta_other"):
+            D.delta_delta_attn_select(shape, kv, inp.q[i], out, sel if name == "delta" else other_sel,
+                                      scratch_idx, scratch_cnt, None, ws, sel_phys=scratch_phys)
         else:
             sd = max(slots[i], 0)
             D.delta_sparse_attn(shape, kv, inp.q[i], out, sel, stack.sel_idx[sd], stack.sel_cnt[sd],
                                 ws, sel_phys=stack.sel_phys[sd])
 
     per_role = {}
-    for name in ("full", "delta", "sparse") + (("delta_fused",) if fused else ()):
-        if (name if name != "delta_fused" else "delta") not in counts:
+    for name in ("full", "delta", "sparse") + (("delta_other",) if other_sel is not None else ()):
+        if (name if name != "delta_other" else "delta") not in counts:
             continue
-        saved_path = os.environ.get("DELTA_DELTA_PATH")
-        if name == "delta_fused":
-            os.environ["DELTA_DELTA_PATH"] = "fused"
         graphs = []
         for si in range(len(sets)):
             s = torch.cuda.Stream()
@@ -260,10 +257,6 @@ def time_layers(D, w, sets, stack, shape, sel, ws, steps, fused=False):
         e1.record()
         torch.cuda.synchronize()
         per_role[name] = e0.elapsed_time(e1) * 1e3 / (steps * len(roles))
-        if saved_path is None:
-            os.environ.pop("DELTA_DELTA_PATH", None)
-        else:
-            os.environ["DELTA_DELTA_PATH"] = saved_path
     return per_role, counts
 
 
@@ -859,17 +852,17 @@ def main():
             delta_bytes += fb
     full_bytes = fb * len(w.roles)
 
-    # the opt-in fused Delta kernel, where it applies to this workload, timed beside the default
-    fused_ok = False
-    if configs.ROLE_DELTA in w.roles and os.environ.get("DELTA_DELTA_PATH") != "fused":
-        os.environ["DELTA_DELTA_PATH"] = "fused"
-        try:
-            fused_ok = D.delta_delta_path(shape, sel)
-        finally:
-            del os.environ["DELTA_DELTA_PATH"]
-    layer_us, per_step = time_layers(D, w, sets, delta_stack, shape, sel, ws, args.steps, fused=fused_ok)
-    fused_us = layer_us.pop("delta_fused", None)
-    log(f"per-launch us: {layer_us}" + (f", fused Delta layer {fused_us:.2f}" if fused_us else ""))
+    # the Delta-layer path the step takes (DELTA_PATH_AUTO), and the other path timed beside it
+    # where both can run on this workload
+    step_fused = D.delta_delta_path(shape, sel)
+    other_sel = D.make_select(w.budget_tokens, w.recent_tokens, w.unit_tokens, D.DELTA_AGG_MAX,
+                              D.DELTA_PATH_SPLIT if step_fused else D.DELTA_PATH_FUSED)
+    if configs.ROLE_DELTA not in w.roles or D.delta_delta_path(shape, other_sel) == step_fused:
+        other_sel = None
+    layer_us, per_step = time_layers(D, w, sets, delta_stack, shape, sel, ws, args.steps, other_sel)
+    other_us = layer_us.pop("delta_other", None)
+    log(f"per-launch us: {layer_us}, Delta path {'fused' if step_fused else 'split'}" +
+        (f", other path {other_us:.2f}" if other_us else ""))
     sb_avg = sum(sparse_bytes) / len(sparse_bytes) if sparse_bytes else 0
     role_bytes = {"full": fb, "delta": fb, "sparse": sb_avg}
     dominant = max(layer_us, key=lambda r: layer_us[r] * per_step[r])
@@ -934,13 +927,15 @@ def main():
         "layer_frac_of_measured_ceiling": {k: round(role_bytes[k] / (layer_us[k] * 1e-6) / 1e9 / ceiling["gbps"], 4)
                                            for k in layer_us},
         "delta_select_overhead": None if overhead is None else round(overhead, 4),
-        "delta_fused_opt_in": None if fused_us is None else {
-            "note": ("Delta layer on the opt-in fused kernel (DELTA_DELTA_PATH=fused), which applies "
-                     "to this shape; the step above uses the default path. One fused workgroup per "
-                     "64-page chunk and sequence: it pays off only when that grid fills the device"),
-            "grid_workgroups": w.batch * math.ceil(math.ceil(max(lens) / 16) / 64),
-            "layer_us": round(fused_us, 2),
-            "delta_select_overhead": round((fused_us - layer_us["full"]) / layer_us["full"], 4)},
+        "delta_path": None if configs.ROLE_DELTA not in w.roles else ("fused" if step_fused else "split"),
+        "delta_other_path": None if other_us is None else {
+            "path": "split" if step_fused else "fused",
+            "note": ("the Delta layer on the path the step does not take (DELTA_PATH_AUTO takes the "
+                     "fused kernel where its grid of one workgroup per 64-page chunk and sequence "
+                     "fills the device and is resident at once), timed the same way"),
+            "grid_workgroups_fused": w.batch * math.ceil(math.ceil(max(lens) / 16) / 64),
+            "layer_us": round(other_us, 2),
+            "delta_select_overhead": round((other_us - layer_us["full"]) / layer_us["full"], 4)},
         "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "bytes_per_launch": int(role_bytes[dominant]),

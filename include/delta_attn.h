@@ -32,8 +32,9 @@
  *   Numerics. bf16 inputs, fp32 accumulation and online softmax, bf16 round-to-nearest-even
  *             outputs.  Results are deterministic: the same inputs and shape give bitwise
  *             identical outputs, and a DELTA layer's attention output is bitwise identical to
- *             delta_full_attn's on the same inputs (with the optional fused DELTA kernel, see
- *             delta_delta_attn_select, the two agree up to floating-point summation order).
+ *             delta_full_attn's on the same inputs when it runs the split path (with the fused
+ *             DELTA kernel, see DELTA_PATH_*, the two agree up to floating-point summation
+ *             order).
  *             FULL and DELTA calls over 2 to 64 sequences split the batch's work evenly over
  *             the GPU from the actual sequence lengths, so a sequence's output bits (never
  *             its accuracy) can depend on the other sequences' lengths in the same call;
@@ -102,7 +103,22 @@ typedef struct {
   int32_t recent_tokens;      /* l: most recent tokens always kept (ceil(l/U) units), >= 0   */
   int32_t unit_tokens;        /* U: 16 (pages) or 1 (tokens)                                  */
   int32_t agg;                /* DELTA_AGG_MAX (paper) or DELTA_AGG_SUM                       */
+  int32_t delta_path;         /* DELTA_PATH_AUTO (0), _SPLIT or _FUSED: how DELTA layers run  */
 } delta_select_t;
+
+/* How a DELTA layer is executed (same selection either way; see delta_delta_attn_select):
+ *   DELTA_PATH_SPLIT  attention (logits staged through the workspace), scoring and selection
+ *                     launches; the layer's attention output is bitwise delta_full_attn's.
+ *   DELTA_PATH_FUSED  one kernel that keeps the logits on chip, wherever it can run: head_dim
+ *                     128, a multiple of 4 KV heads, at most 32 query heads, at most 2048
+ *                     candidate units and a grid of ceil(max_seq_len / 1024) x batch workgroups
+ *                     that the device holds at once; elsewhere the split launches.  Its output
+ *                     equals delta_full_attn's up to floating-point summation order (within the
+ *                     bf16 rounding of the result), not bit for bit.
+ *   DELTA_PATH_AUTO   the fused kernel where it can run and its grid also fills the device (at
+ *                     least one workgroup per CU), which is where it is the faster of the two on
+ *                     MI355X; the split launches elsewhere.  */
+enum { DELTA_PATH_AUTO = 0, DELTA_PATH_SPLIT = 1, DELTA_PATH_FUSED = 2 };
 
 /* Bytes of workspace needed by every call with this shape (and, if non-NULL, these selection
  * parameters; pass the same `sel` used for DELTA and SPARSE calls).  Host only. */
@@ -119,7 +135,7 @@ int delta_workspace_init(void* ws, size_t ws_bytes, void* stream);
 int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void* q, void* out,
                     void* ws, size_t ws_bytes, void* stream);
 
-/* DELTA role: the FULL computation (bitwise-identical `out`), then RefreshPages (App. A,
+/* DELTA role: the FULL computation (the same `out`; see DELTA_PATH_*), then RefreshPages (App. A,
  * Alg. 2): token score s_t = max over all m heads of softmax weight (Sec. 4), unit score
  * S_u = sum of s_t over the U tokens of unit u (a partial last unit sums the tokens it has),
  * and the selected set = the last L units plus the top-(K-L) of the older units by S_u,
@@ -134,25 +150,24 @@ int delta_full_attn(const delta_shape_t* shape, const delta_kv_t* kv, const void
  *                NULL: not written.
  *   unit_scores: optional fp32 [B, ceil(max_seq_len / U)]: S_u for u < ceil(seq_lens[b]/U);
  *                NULL keeps them in the workspace.
- * Launches: the attention kernel (which stages the logits through the workspace), a scoring
- * kernel and a selection kernel.  With DELTA_DELTA_PATH=fused in the environment, shapes with
- * head_dim 128, a multiple of 4 KV heads, at most 32 query heads, at most 2048 candidate units
- * and a grid the device holds at once instead run one kernel that keeps the logits on chip
- * (opt-in: on MI355X it is faster only where its grid fills the device, e.g. 101 vs 105 us
- * per layer for 8 sequences of 32K tokens with 28 query and 4 KV heads; its `out` agrees with
- * delta_full_attn's up to summation order, not bit for bit).  Its workgroups wait
- * for the rest of their sequence for at most DELTA_FUSED_SPIN_TICKS ticks of the 100 MHz clock
- * (default 1 ms) and then hand their part to the sequence's last workgroup, so it never
- * hangs when not all of them are resident, and gives the same results either way. */
+ * Launches, by sel->delta_path: the split path runs the attention kernel (which stages the
+ * logits through the workspace), a scoring kernel and a selection kernel; the fused path one
+ * kernel that keeps the logits on chip (with DELTA_PATH_AUTO, e.g. 8 sequences of 32K tokens
+ * with 28 query and 4 KV heads, where its 256 workgroups fill the 256 CUs).  The fused kernel's
+ * workgroups wait for the rest of their sequence for at most DELTA_FUSED_SPIN_TICKS ticks of the
+ * 100 MHz clock (environment, default 1 ms) and then hand their part to the sequence's last
+ * workgroup, so it never hangs when not all of them are resident, and gives the same results
+ * either way. */
 int delta_delta_attn_select(const delta_shape_t* shape, const delta_kv_t* kv, const void* q,
                             void* out, const delta_select_t* sel, int32_t* sel_idx,
                             int32_t* sel_cnt, int32_t* sel_phys, float* unit_scores, void* ws,
                             size_t ws_bytes, void* stream);
 
-/* Which path delta_delta_attn_select takes for this shape and selection under the current
- * environment and device: *fused = 1 for the fused kernel (see above), 0 for the attention,
- * scoring and selection launches.  Host only; it queries the current device's occupancy for
- * the fused kernel.  Errors as delta_workspace_bytes; `sel` and `fused` must be non-NULL. */
+/* Which path delta_delta_attn_select takes for this shape and selection (sel->delta_path) on
+ * the current device: *fused = 1 for the fused kernel, 0 for the attention, scoring and
+ * selection launches.  Host only; it queries the current device's CU count and its occupancy
+ * for the fused kernel (without a device: 0 unless the kernel cannot apply anyway).  Errors as
+ * delta_workspace_bytes; `sel` and `fused` must be non-NULL. */
 int delta_delta_path(const delta_shape_t* shape, const delta_select_t* sel, int* fused);
 
 /* SPARSE role: attention of each query over the tokens of the selected units only, the

@@ -114,6 +114,9 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   __shared__ float s_m[kWaves][kMaxGroup], s_l[kWaves][kMaxGroup];
   __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][D];
   __shared__ int s_last;
+#if DELTA_QK_VALU
+  __shared__ __attribute__((aligned(16))) uint16_t s_qv[kWaves][G * D];
+#endif
   static_assert(G * D <= 4 * kAttnThreads && D % 4 == 0, "four outputs per thread cover a group");
 
   // ---- attention of groups [g0, g0 + ng) of (sequence b, KV head g), staged by stage(); the
@@ -166,9 +169,19 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     // the K/V read stream cost several times their bytes, while the same bytes written in a
     // few large streaming bursts (reads paused) cost about their share.  A chunk is a multiple
     // of 16 groups.
+#if DELTA_QK_VALU
+    // build option: QK^T on the vector ALUs, the query vectors read from the wave's LDS copy
+    stage_query_lds<D, G>(qb, s_qv[wave], lane);
+    wave_lds_sync();
+    auto process = [&](const Tile<D>& t, int slot_in_chunk) {
+      process_tile_valu<D, G, LOGITS>(t, s_qv[wave], a.scale_log2, st, lp,
+                                      s_stage + slot_in_chunk * G * 16, lane);
+    };
+#else
     auto process = [&](const Tile<D>& t, int slot_in_chunk) {
       process_tile<D, G, LOGITS>(t, qb, a.scale_log2, st, lp, s_stage + slot_in_chunk * G * 16, lane);
     };
+#endif
 
     // Waves interleave in blocks of four groups (wave w takes groups 16j + 4w .. 16j + 4w + 3),
     // so the workgroup streams about sixteen adjacent pages at a time.  A wave walks its groups

@@ -112,19 +112,16 @@ __device__ __forceinline__ void load_page_tile(Tile<D>& t, const uint16_t* kt, c
   for (int i = 0; i < Gm::NI; ++i) t.v[i] = load16_stream(vp + (real ? (size_t)Gm::RPI * i * D : 0));
 }
 
-// Folds one tile into the wave's softmax state.  lp: the wave's LDS slice (16 x 8 + 8 floats).
-// With LOGITS, the tile's scaled log2-domain logits go to logit_slot[head][16] (LDS).
+// Folds one tile's score tile (acc: lane (quad, hcol) holds q_hcol . k_r for rows
+// r = 4*quad .. 4*quad+3, unscaled) into the wave's softmax state.  lp: the wave's LDS slice
+// (16 x 8 + 8 floats).  With LOGITS, the tile's scaled log2-domain logits go to
+// logit_slot[head][16] (LDS).
 template <int D, int G, bool LOGITS>
-__device__ __forceinline__ void process_tile(const Tile<D>& t, const bf16x8 (&qb)[Geo<D>::NK],
-                                             float scale_log2, WaveSoftmax<G>& st, float* lp,
-                                             float* logit_slot, int lane) {
+__device__ __forceinline__ void fold_tile(const f32x4 acc, const Tile<D>& t, float scale_log2,
+                                          WaveSoftmax<G>& st, float* lp, float* logit_slot,
+                                          int lane) {
   using Gm = Geo<D>;
   const int quad = lane >> 4, hcol = lane & 15;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < Gm::NK; ++ks)
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.k[ks]), qb[ks],
-                                                  acc, 0, 0, 0);
   float x[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r)
@@ -181,6 +178,73 @@ __device__ __forceinline__ void process_tile(const Tile<D>& t, const bf16x8 (&qb
       for (int e = 0; e < 8; ++e) st.o[h][e] = fmaf(ph, v[e], st.o[h][e]);
     }
   }
+}
+
+// Folds one tile into the wave's softmax state, QK^T on the matrix cores (see the file header).
+template <int D, int G, bool LOGITS>
+__device__ __forceinline__ void process_tile(const Tile<D>& t, const bf16x8 (&qb)[Geo<D>::NK],
+                                             float scale_log2, WaveSoftmax<G>& st, float* lp,
+                                             float* logit_slot, int lane) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < Geo<D>::NK; ++ks)
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.k[ks]), qb[ks],
+                                                  acc, 0, 0, 0);
+  fold_tile<D, G, LOGITS>(acc, t, scale_log2, st, lp, logit_slot, lane);
+}
+
+// The same score tile with QK^T on the vector ALUs, a build option (DELTA_QK_VALU) kept for
+// comparing the two engines.  Lane (quad, r) holds 32 head-dim values of K row r (the registers
+// of the matrix-core operand) and forms their dot products with the same 32 values of every
+// query head (sq: the wave's LDS copy of the G query vectors, bf16 [G][D]) with
+// v_dot2_f32_bf16; the four quads' partial sums are added across lanes, and the tile goes
+// through the wave's LDS slice into the matrix-core layout that fold_tile reads.
+template <int D, int G>
+__device__ __forceinline__ void stage_query_lds(const bf16x8 (&qb)[Geo<D>::NK], uint16_t* sq,
+                                                int lane) {
+  const int quad = lane >> 4, hcol = lane & 15;
+  if (hcol < G) {
+#pragma unroll
+    for (int ks = 0; ks < Geo<D>::NK; ++ks)
+      *reinterpret_cast<bf16x8*>(sq + hcol * D + 32 * ks + 8 * quad) = qb[ks];
+  }
+}
+
+template <int D, int G, bool LOGITS>
+__device__ __forceinline__ void process_tile_valu(const Tile<D>& t, const uint16_t* sq,
+                                                  float scale_log2, WaveSoftmax<G>& st, float* lp,
+                                                  float* logit_slot, int lane) {
+  const int quad = lane >> 4, r = lane & 15;
+  float part[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) part[h] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < Geo<D>::NK; ++ks) {
+    const u32x4 kw = t.k[ks];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const u32x4 qw = *reinterpret_cast<const u32x4*>(sq + h * D + 32 * ks + 8 * quad);
+      // v_dot2_f32_bf16 written out: with hipcc of ROCm 7.2 at -O3 the builtin
+      // (__builtin_amdgcn_fdot2_f32_bf16) compiled to the same operand pair repeated for the
+      // four pairs of a 16-byte chunk (wrong sums; found with a one-tile check against the
+      // matrix-core tile), the instruction itself gives the right ones
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        asm volatile("v_dot2_f32_bf16 %0, %1, %2, %0" : "+v"(part[h]) : "v"(kw[c]), "v"(qw[c]));
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h) part[h] = sum_xor32(sum_xor16(part[h]));
+  wave_lds_sync();
+  if (quad == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) lp[r * 8 + h] = part[h];
+  }
+  wave_lds_sync();
+  f32x4 acc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = r < G ? lp[(4 * quad + i) * 8 + r] : 0.f;
+  fold_tile<D, G, LOGITS>(acc, t, scale_log2, st, lp, logit_slot, lane);
 }
 
 // Sums each lane's output share over the lanes that hold the same head-dim columns: afterwards

@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/delta_attn.h"
 #include "internal.h"
@@ -156,6 +157,9 @@ int check_select(const delta_select_t* sel) {
   if (!sel) return DELTA_ERR_INVALID_ARG;
   if (sel->unit_tokens != 16 && sel->unit_tokens != 1) return DELTA_ERR_UNSUPPORTED;
   if (sel->agg != DELTA_AGG_MAX && sel->agg != DELTA_AGG_SUM) return DELTA_ERR_INVALID_ARG;
+  if (sel->delta_path != DELTA_PATH_AUTO && sel->delta_path != DELTA_PATH_SPLIT &&
+      sel->delta_path != DELTA_PATH_FUSED)
+    return DELTA_ERR_INVALID_ARG;
   if (sel->budget_tokens < 1 || sel->recent_tokens < 0) return DELTA_ERR_INVALID_ARG;
   if (sel->budget_tokens % sel->unit_tokens) return DELTA_ERR_INVALID_ARG;
   // L < K, counted in units (a window that rounds up to the whole budget leaves no choice);
@@ -262,17 +266,17 @@ int run_full(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* 
                                  s->batch, st));
 }
 
-// `phys` (nullable): where the select kernel also writes the physical location of every
-// selected unit, read through this layer's page table.
 // Whether a Delta layer runs as one fused launch (logits kept in LDS) instead of attention +
 // scoring + selection launches.  The fused kernel needs head_dim 128, a multiple of 4 KV
 // heads, at most kFusedMaxQHeads query heads, at most 2048 selection candidates, and its grid
-// of (chunks x sequences) must fit on the device at once (otherwise its sequence barrier would
-// mostly run into its time limit and fall back to the slow path).  DELTA_DELTA_PATH=split or
-// =fused in the environment forces either path where the fused kernel applies.
+// of (chunks x sequences) must be resident on the device at once (otherwise its sequence
+// barrier would mostly run into its time limit and fall back to the slow path).  It pays off
+// only when that grid also fills the device, one workgroup per CU or more: then every CU
+// streams and the fused kernel saves the logit round trip and two launches; a smaller grid
+// leaves CUs idle that the split attention launch would use.  sel->delta_path picks: SPLIT
+// never, FUSED wherever it can run, AUTO where it can run and fills the device.
 bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const Layout& L) {
-  const char* e = getenv("DELTA_DELTA_PATH");
-  if (!e || strcmp(e, "fused")) return false;
+  if (sel->delta_path == DELTA_PATH_SPLIT) return false;
   const int G = s->n_q_heads / s->n_kv_heads;
   if (s->head_dim != 128 || s->n_kv_heads % 4 != 0 || s->n_q_heads > kFusedMaxQHeads) return false;
   const int n_c = L.nu_stride - recent_units_of(sel);
@@ -281,18 +285,25 @@ bool use_fused_delta(const delta_shape_t* s, const delta_select_t* sel, const La
   const int64_t grid = (int64_t)L.fused_chunks * s->batch;
   const int64_t part_bytes = (int64_t)s->batch * s->n_q_heads * L.fused_chunks * s->head_dim * 4;
   if (part_bytes > 0x7fffffff) return false;
-  // capacity per device, group size and unit size, measured once
+  // resident capacity per device, group size and unit size, and the device's CU count,
+  // measured once
+  static std::mutex mu;
   static int cache[64][kMaxGroup + 1][2];
-  static bool filled[64][kMaxGroup + 1][2];
+  static int cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
   const int ui = sel->unit_tokens == 16 ? 0 : 1;
-  if (!filled[dev][G][ui]) {
-    cache[dev][G][ui] = fused_delta_capacity(s->head_dim, G, sel->unit_tokens);
-    filled[dev][G][ui] = true;
+  int cap = 0, n_cu = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (!cache[dev][G][ui]) cache[dev][G][ui] = 1 + fused_delta_capacity(s->head_dim, G, sel->unit_tokens);
+    if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus[dev] = 0;
+    cap = cache[dev][G][ui] - 1;
+    n_cu = cus[dev];
   }
-  const int cap = cache[dev][G][ui];
-  return grid <= cap;
+  if (grid > cap) return false;
+  return sel->delta_path == DELTA_PATH_FUSED || (n_cu > 0 && grid >= n_cu);
 }
 
 // Longest wait of a fused-kernel workgroup at its sequence barrier: 1 ms of the 100 MHz
@@ -306,6 +317,9 @@ int64_t fused_spin_ticks() {
   return e ? std::max<int64_t>(0, atoll(e)) : (int64_t)100000;
 }
 
+// A Delta layer: the fused kernel, or attention (logits on), scoring and selection.  `phys`
+// (nullable): where the selection also writes the physical location of every selected unit,
+// read through this layer's page table.
 int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void* out,
               const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt, float* uscores,
               int32_t* phys, const Layout& L, char* ws, hipStream_t st) {

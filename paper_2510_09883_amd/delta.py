@@ -22,6 +22,7 @@ DELTA_OK, DELTA_ERR_INVALID_ARG, DELTA_ERR_UNSUPPORTED, DELTA_ERR_WORKSPACE, DEL
 DELTA_ERR_HOOK = -5
 DELTA_ROLE_FULL, DELTA_ROLE_DELTA, DELTA_ROLE_SPARSE = 0, 1, 2
 DELTA_AGG_MAX, DELTA_AGG_SUM = 0, 1
+DELTA_PATH_AUTO, DELTA_PATH_SPLIT, DELTA_PATH_FUSED = 0, 1, 2
 
 EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
             "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
@@ -44,7 +45,8 @@ class delta_kv_t(ctypes.Structure):
 
 class delta_select_t(ctypes.Structure):
     _fields_ = [("budget_tokens", ctypes.c_int32), ("recent_tokens", ctypes.c_int32),
-                ("unit_tokens", ctypes.c_int32), ("agg", ctypes.c_int32)]
+                ("unit_tokens", ctypes.c_int32), ("agg", ctypes.c_int32),
+                ("delta_path", ctypes.c_int32)]
 
 
 _P = ctypes.POINTER
@@ -166,8 +168,9 @@ def make_shape(batch, n_q_heads, n_kv_heads, head_dim, max_pages_per_seq, max_se
                          max_seq_len, sm_scale)
 
 
-def make_select(budget_tokens, recent_tokens, unit_tokens=16, agg=DELTA_AGG_MAX) -> delta_select_t:
-    return delta_select_t(budget_tokens, recent_tokens, unit_tokens, agg)
+def make_select(budget_tokens, recent_tokens, unit_tokens=16, agg=DELTA_AGG_MAX,
+                delta_path=DELTA_PATH_AUTO) -> delta_select_t:
+    return delta_select_t(budget_tokens, recent_tokens, unit_tokens, agg, delta_path)
 
 
 def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
@@ -180,8 +183,8 @@ def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
 
 
 def delta_delta_path(shape: delta_shape_t, sel: delta_select_t) -> bool:
-    """Whether delta_delta_attn_select runs the fused kernel for this shape and selection under
-    the current environment (DELTA_DELTA_PATH) and device."""
+    """Whether delta_delta_attn_select runs the fused kernel for this shape and selection
+    (sel.delta_path) on the current device."""
     f = ctypes.c_int(0)
     _check("delta_delta_path", _lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(sel),
                                                      ctypes.byref(f)))

@@ -30,9 +30,10 @@ def shape_of(inp, sm_scale=0.0):
                           inp.max_seq_len, sm_scale)
 
 
-def select_of(w, agg=0, budget=None, recent=None):
+def select_of(w, agg=0, budget=None, recent=None, path=0):
     return D().make_select(w.budget_tokens if budget is None else budget,
-                           w.recent_tokens if recent is None else recent, w.unit_tokens, agg)
+                           w.recent_tokens if recent is None else recent, w.unit_tokens, agg,
+                           path)
 
 
 class StepResult:
@@ -40,13 +41,14 @@ class StepResult:
         self.outs, self.sel_idx, self.sel_cnt = outs, sel_idx, sel_cnt
 
 
-def run_step(inp, roles=None, agg=0, budget=None, recent=None, ws=None):
-    """One decoding step of the whole stack through delta_decode_step."""
+def run_step(inp, roles=None, agg=0, budget=None, recent=None, ws=None, path=0):
+    """One decoding step of the whole stack through delta_decode_step (path: the Delta-layer
+    path, DELTA_PATH_AUTO by default)."""
     d = D()
     w = inp.workload
     roles = w.roles if roles is None else roles
     shape = shape_of(inp)
-    sel = select_of(w, agg, budget, recent)
+    sel = select_of(w, agg, budget, recent, path)
     if ws is None:
         ws = d.alloc_workspace(shape, sel)
     outs = [torch.full_like(inp.q[i], float("nan")) for i in range(len(roles))]

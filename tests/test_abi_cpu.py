@@ -225,15 +225,21 @@ def test_binding_refuses_host_and_mistyped_buffers(D):
         D._check_sel(s, sel, torch.zeros((1, 3), dtype=torch.int32), torch.zeros((1,), dtype=torch.int32))
 
 
-def test_delta_path_query(D, monkeypatch):
-    """Without DELTA_DELTA_PATH=fused the split path is reported; bad arguments are refused."""
-    monkeypatch.delenv("DELTA_DELTA_PATH", raising=False)
+def test_delta_path_query(D):
+    """The Delta-layer path is a field of the selection parameters: SPLIT is always the split
+    path, AUTO and FUSED need a device to measure (none here: split); a bad value and bad
+    arguments are refused."""
     shape = D.make_shape(8, 28, 4, 128, 2048, 32768)
+    for path in (D.DELTA_PATH_AUTO, D.DELTA_PATH_SPLIT, D.DELTA_PATH_FUSED):
+        assert D.delta_delta_path(shape, D.make_select(2048, 128, 16, 0, path)) is False
     sel = D.make_select(2048, 128, 16, 0)
-    assert D.delta_delta_path(shape, sel) is False
     f = ctypes.c_int(7)
     assert D._lib.delta_delta_path(ctypes.byref(shape), None, ctypes.byref(f)) == D.DELTA_ERR_INVALID_ARG
     assert D._lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(sel), None) == D.DELTA_ERR_INVALID_ARG
     bad = D.make_select(2048, 4096, 16, 0)   # recency window not below the budget
     assert D._lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(bad), ctypes.byref(f)) == D.DELTA_ERR_INVALID_ARG
+    bad_path = D.make_select(2048, 128, 16, 0, 3)
+    assert D._lib.delta_delta_path(ctypes.byref(shape), ctypes.byref(bad_path), ctypes.byref(f)) == D.DELTA_ERR_INVALID_ARG
+    with pytest.raises(D.DeltaError):
+        D.delta_workspace_bytes(shape, bad_path)
     assert f.value == 7
