@@ -89,6 +89,8 @@ typedef struct {
   const void* v_cache;        /* bf16, same layout                                            */
   const int32_t* page_table;  /* int32 [batch, max_pages_per_seq]                             */
   const int32_t* seq_lens;    /* int32 [batch]: tokens cached, the current one included       */
+  int64_t n_pages;            /* n_phys_pages, or 0 if not stated; read by the debug build's
+                                 checks of page-table entries only                           */
 } delta_kv_t;
 
 /* Selection parameters (Sec. 4; App. A, Alg. 2).  All counts are in TOKENS.  The budget must
@@ -256,6 +258,21 @@ int delta_decode_step_noalloc(const delta_shape_t* shape, int32_t n_layers, cons
                               const delta_kv_t* kv, const void* const* q, void* const* out,
                               const delta_select_t* sel, int32_t* sel_idx, int32_t* sel_cnt,
                               void* stream);
+
+/* Build information: DELTA_BUILD_DEBUG is set in a library built with -DDELTA_DEBUG=1
+ * (python -m paper_2510_09883_amd.build --debug: libdelta_attn_debug.so).  A debug build checks
+ * on the device the preconditions that release builds only document: every page-table entry
+ * and physical location it reads lies in [0, kv->n_pages) (only >= 0 when n_pages is 0), every
+ * seq_lens[b] in [1, max_seq_len], every selected unit inside its sequence.  A failed check ORs
+ * a DELTA_DEBUG_* bit into the 32-bit word at byte 0 of the workspace and the kernel goes on
+ * with an in-range value (physical page 0, the length clamped, the unit masked), so it never
+ * reads outside the caller's buffers; results are then meaningless but defined.  The word is
+ * zero after delta_workspace_init; the caller reads it after synchronising the stream.  Release
+ * builds never write it.  delta_kv_append has no workspace: in a debug build it skips a
+ * sequence whose page-table entry fails the check. */
+enum { DELTA_BUILD_DEBUG = 1 };
+enum { DELTA_DEBUG_PAGE = 1, DELTA_DEBUG_SEQ_LEN = 2, DELTA_DEBUG_SELECTION = 4 };
+int delta_build_flags(void);
 
 /* Static description of a status code. */
 const char* delta_status_string(int status);

@@ -1,6 +1,8 @@
 """Build the gfx950 HIP library libdelta_attn.so in-tree (hipcc, no PyTorch extension machinery).
 
-    python -m paper_2510_09883_amd.build        # or __graft_entry__.build()
+    python -m paper_2510_09883_amd.build            # or __graft_entry__.build()
+    python -m paper_2510_09883_amd.build --debug    # libdelta_attn_debug.so: device-side checks
+    python -m paper_2510_09883_amd.build -DNAME=1   # extra compiler flags (build options)
 """
 from __future__ import annotations
 
@@ -13,6 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdelta_attn.so")
+DEBUG_LIB = os.path.join(PKG, "libdelta_attn_debug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["attn_kernel.hip", "fused_delta_kernel.hip", "select_kernel.hip", "append_kernel.hip",
@@ -34,25 +37,31 @@ def _compile(src: str, obj: str, extra):
     return r.stderr
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    """Compile every source for gfx950 and link the shared library. Returns its path."""
-    out_dir = os.path.join(PKG, "_build")
+def build(verbose: bool = False, extra=(), debug: bool = False) -> str:
+    """Compile every source for gfx950 and link the shared library. Returns its path.  With
+    debug, the kernels check their device-side preconditions (-DDELTA_DEBUG=1) and the library
+    is libdelta_attn_debug.so."""
+    out_dir = os.path.join(PKG, "_build", "debug") if debug else os.path.join(PKG, "_build")
+    lib = DEBUG_LIB if debug else LIB
+    extra = list(extra) + (["-DDELTA_DEBUG=1"] if debug else [])
     os.makedirs(out_dir, exist_ok=True)
     objs = [os.path.join(out_dir, s.rsplit(".", 1)[0] + ".o") for s in SOURCES]
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         logs = list(ex.map(lambda so: _compile(so[0], so[1], list(extra)), zip(SOURCES, objs)))
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
         for s, log in zip(SOURCES, logs):
             if log.strip():
                 print(f"--- {s}\n{log}", file=sys.stderr)
-    return LIB
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose=True, extra=sys.argv[1:]))
+    args = sys.argv[1:]
+    dbg = "--debug" in args
+    print(build(verbose=True, extra=[a for a in args if a != "--debug"], debug=dbg))

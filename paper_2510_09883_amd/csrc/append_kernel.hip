@@ -19,6 +19,8 @@ __global__ __launch_bounds__(kAppendThreads) void kv_append_kernel(const AppendA
   if (s < 1 || s > 16 * a.max_pages) return;   // no token slot: nothing written
   const int t = s - 1;
   const int page = a.page_table[(size_t)b * a.max_pages + (t >> 4)];
+  // debug builds: a page outside the cache is not written (there is no status word to flag it)
+  if (DELTA_DEBUG && (page < 0 || (a.n_pages > 0 && page >= a.n_pages))) return;
   const int row = t & 15;
   const int per_row = a.head_dim / 8;             // 16-byte pieces of one head's row
   const int chunks = a.n_kv_heads * per_row;      // of the K (or V) row over all heads

@@ -36,6 +36,7 @@
 // outputs (and the log-sum-exp), and re-arms the counter to zero for the next launch.  A pair
 // that is one piece skips all of this and has its outputs written directly.
 #include "attn_tile.h"
+#include "debug_check.h"
 #include "internal.h"
 #include "wave.h"
 
@@ -69,11 +70,16 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   bf16x8 qb[Gm::NK];
   __shared__ int s_rows[kMaxRowSlots];
   __shared__ int s_aux[MODE == ROWS_SEL_PAGE ? kMaxRowSlots : 1];
+  // (Debug builds check every physical page and selected unit here and flag bad ones; see
+  // checked_page.)
   auto stage = [&](int b, int g, int g0, int cand) {
     load_query<D, G>(qb, a.q, (size_t)b * Hq + g * G, lane);
     const int32_t* pt = a.page_table + (size_t)b * a.max_pages;
+    // debug builds: the sequence's length bounds its selected units (release: unused)
+    const int s_dbg = DELTA_DEBUG && MODE != ROWS_DENSE ? a.seq_lens[b] : 0;
     if (MODE == ROWS_DENSE) {
-      for (int i = tid; i < cand; i += kAttnThreads) s_rows[i] = pt[g0 + i];
+      for (int i = tid; i < cand; i += kAttnThreads)
+        s_rows[i] = checked_page(pt[g0 + i], a.n_pages, a.status);
     } else if (MODE == ROWS_SEL_PAGE) {
       // with precomputed physical pages the index and the page arrive together
       const int32_t* sel = a.sel_idx + (size_t)b * a.sel_stride;
@@ -82,7 +88,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
         const int u = sel[g0 + i];
         const int ph = phys ? phys[g0 + i] : 0;
         const bool ok = u >= 0 && u < a.max_pages;
-        s_rows[i] = ok ? (phys ? ph : pt[u]) : 0;
+        if (DELTA_DEBUG && u >= 0 && 16 * u >= s_dbg) debug_flag(a.status, DELTA_DEBUG_SELECTION);
+        s_rows[i] = ok ? checked_page(phys ? ph : pt[u], a.n_pages, a.status) : 0;
         s_aux[i] = ok ? u : 0;
       }
     } else {
@@ -94,7 +101,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
         if (i < n_rows) {
           const int t = sel[16 * g0 + i];
           const int ph = phys ? phys[16 * g0 + i] : 0;
-          if (t >= 0 && t < 16 * a.max_pages) packed = phys ? ph : pt[t >> 4] * 16 + (t & 15);
+          if (DELTA_DEBUG && t >= s_dbg) debug_flag(a.status, DELTA_DEBUG_SELECTION);
+          if (t >= 0 && t < 16 * a.max_pages) {
+            const int page = checked_page(phys ? ph >> 4 : pt[t >> 4], a.n_pages, a.status);
+            packed = page * 16 + (phys ? ph & 15 : t & 15);
+          }
         }
         s_rows[i] = packed;
       }
@@ -371,6 +382,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
   const int cand_s = max(0, min(a.gps, a.max_groups - g0_s));
   stage(b_s, g_s, g0_s, cand_s);
   const int s_bs = a.seq_lens[b_s];
+  if (DELTA_DEBUG && (s_bs < 1 || s_bs > a.max_seq_len) && tid == 0 && blockIdx.x == 0 && blockIdx.y == 0)
+    debug_flag(a.status, DELTA_DEBUG_SEQ_LEN);
   const int sel_ns = (MODE == ROWS_DENSE) ? 0 : min(a.sel_cnt[b_s], a.sel_stride);
 
   int bal_chunk = 0;          // > 0: this launch takes the balanced decomposition

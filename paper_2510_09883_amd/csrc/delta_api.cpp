@@ -120,7 +120,7 @@ void plan_balance(int batch, int pairs, SplitPlan* p) {
 }
 
 struct Layout {
-  size_t counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, phys = 0;
+  size_t status = 0, counters = 0, part_ml = 0, part_o = 0, logits = 0, lse = 0, uscores = 0, phys = 0;
   size_t fcnt = 0, fflag = 0;
   size_t total = 0;
   int fused_chunks = 0;   // chunks per sequence of the fused Delta kernel
@@ -203,6 +203,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     part_splits = std::max(part_splits, L->fused_chunks);
   }
   size_t off = 0;
+  L->status = off;    off = align_up(off + sizeof(uint32_t));   // debug builds' status word
   L->counters = off;  off = align_up(off + sizeof(int32_t) * pairs);
   L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * 2);
   L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * s->head_dim);
@@ -220,7 +221,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
 }
 
 int check_kv(const delta_kv_t* kv) {
-  if (!kv || !kv->k_cache || !kv->v_cache || !kv->page_table || !kv->seq_lens)
+  if (!kv || !kv->k_cache || !kv->v_cache || !kv->page_table || !kv->seq_lens || kv->n_pages < 0)
     return DELTA_ERR_INVALID_ARG;
   return DELTA_OK;
 }
@@ -254,6 +255,9 @@ AttnArgs base_args(const delta_shape_t* s, const delta_kv_t* kv, const void* q, 
   a.chunk_min = plan.chunk_min;
   a.balance = plan.balance;
   a.scale_log2 = scale_log2(s);
+  a.n_pages = kv->n_pages;
+  a.max_seq_len = s->max_seq_len;
+  a.status = reinterpret_cast<uint32_t*>(ws + L.status);
   return a;
 }
 
@@ -360,6 +364,8 @@ int run_delta(const delta_shape_t* s, const delta_kv_t* kv, const void* q, void*
     f.agg = sel->agg;
     f.scale_log2 = scale_log2(s);
     f.sel = xa;
+    f.n_pages = kv->n_pages;
+    f.status = reinterpret_cast<uint32_t*>(ws + L.status);
     return hip_rc(launch_fused_delta(s->head_dim, s->n_q_heads / s->n_kv_heads, f, s->batch, st));
   }
   AttnArgs a = base_args(s, kv, q, out, L, ws, L.dense);
@@ -544,6 +550,7 @@ int delta_kv_append(const delta_shape_t* shape, void* k_cache, void* v_cache,
   a.n_kv_heads = shape->n_kv_heads;
   a.head_dim = shape->head_dim;
   a.max_pages = shape->max_pages_per_seq;
+  a.n_pages = 0;   // no cache descriptor: the debug build checks the sign only
   return launch_kv_append(a, shape->batch, static_cast<hipStream_t>(stream)) == hipSuccess
              ? DELTA_OK : DELTA_ERR_HIP;
 }
@@ -586,11 +593,14 @@ int delta_decode_step_noalloc(const delta_shape_t* shape, int32_t n_layers, cons
   hipStream_t st = static_cast<hipStream_t>(stream);
   const size_t pairs = (size_t)shape->batch * shape->n_kv_heads;
   const size_t fused_bytes = L.fcnt ? L.total - L.fcnt : 0;   // fused counters and chunk flags
-  if (launch_fill_zero2(w + L.counters, sizeof(int32_t) * pairs, w + L.fcnt, fused_bytes, st) != hipSuccess)
+  // (from byte 0: the debug builds' status word, then the counters)
+  if (launch_fill_zero2(w, L.counters + sizeof(int32_t) * pairs, w + L.fcnt, fused_bytes, st) != hipSuccess)
     return DELTA_ERR_HIP;
   return enqueue_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, L, w, stream,
                       nullptr);
 }
+
+int delta_build_flags(void) { return DELTA_DEBUG ? DELTA_BUILD_DEBUG : 0; }
 
 const char* delta_status_string(int status) {
   switch (status) {

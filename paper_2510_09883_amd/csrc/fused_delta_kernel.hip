@@ -27,6 +27,7 @@
 #include <type_traits>
 
 #include "attn_tile.h"
+#include "debug_check.h"
 #include "internal.h"
 #include "select_impl.h"
 #include "wave.h"
@@ -69,7 +70,9 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
   __shared__ __attribute__((aligned(16))) float s_logit[kFusedMaxQHeads * kC * 16];
   __shared__ float s_M[kFusedMaxQHeads], s_L[kFusedMaxQHeads], s_lse[kFusedMaxQHeads];
   __shared__ int s_last;
-  if (tid < np) s_pages[tid] = a.page_table[(size_t)b * a.max_pages + p0 + tid];
+  if (tid < np) s_pages[tid] = checked_page(a.page_table[(size_t)b * a.max_pages + p0 + tid], a.n_pages, a.status);
+  if (DELTA_DEBUG && c == 0 && tid == 0 && (a.seq_lens[b] < 1 || a.seq_lens[b] > a.max_seq_len))
+    debug_flag(a.status, DELTA_DEBUG_SEQ_LEN);
   float* lp = s_p[wave];
 
   const size_t part_rows = (size_t)gridDim.y * Hkv * a.n_chunks * G;   // rows of G x D / G x 2

@@ -4,6 +4,15 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/delta_attn.h"
+
+// Debug builds (-DDELTA_DEBUG=1) check on the device the preconditions that the host cannot see
+// (page-table entries, sequence lengths, selected units; see delta_build_flags in the C ABI),
+// record a failure as a bit in the workspace's status word and go on with an in-range value.
+#ifndef DELTA_DEBUG
+#define DELTA_DEBUG 0
+#endif
+
 namespace delta {
 
 // How the 16-row groups an attention workgroup walks are formed.
@@ -45,6 +54,9 @@ struct AttnArgs {
   int32_t chunk_min;         // shortest run of the balanced decomposition (dense launches)
   int32_t balance;           // 1: a dense launch may take the balanced decomposition
   float scale_log2;          // sm_scale * log2(e)
+  int64_t n_pages;           // physical pages of the caches (0: not stated); debug checks
+  int32_t max_seq_len;       // host bound of seq_lens[b]; debug checks
+  uint32_t* status;          // debug status word (workspace byte 0)
 };
 
 hipError_t launch_attention(int head_dim, int group, int mode, const AttnArgs& a, int batch,
@@ -101,6 +113,8 @@ struct FusedArgs {
   int32_t n_q_heads, n_kv_heads, max_pages, n_chunks, max_seq_len, agg, logit_pages;
   float scale_log2;
   SelectArgs sel;            // unit scores (written here), selection outputs
+  int64_t n_pages;           // physical pages of the caches (0: not stated); debug checks
+  uint32_t* status;          // debug status word (workspace byte 0)
 };
 
 // Largest grid (chunks x sequences) the fused kernel can have resident at once on the current
@@ -119,6 +133,7 @@ struct AppendArgs {
   const uint16_t* v_new;
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
   int32_t n_kv_heads, head_dim, max_pages;
+  int64_t n_pages;           // physical pages of the caches (0: not stated); debug checks
 };
 
 hipError_t launch_kv_append(const AppendArgs& a, int batch, hipStream_t stream);

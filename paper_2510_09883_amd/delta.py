@@ -12,7 +12,9 @@ import os
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdelta_attn.so")
+# DELTA_ATTN_LIB selects another build of the same library (the debug or host-ASan build)
+LIB_PATH = os.environ.get("DELTA_ATTN_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libdelta_attn.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                       "(python -m paper_2510_09883_amd.build)")
@@ -27,7 +29,9 @@ DELTA_PATH_AUTO, DELTA_PATH_SPLIT, DELTA_PATH_FUSED = 0, 1, 2
 EXPORTED = ["delta_workspace_bytes", "delta_workspace_init", "delta_full_attn",
             "delta_delta_attn_select", "delta_sparse_attn", "delta_decode_step",
             "delta_kv_append", "delta_decode_step_hooked", "delta_delta_path",
-            "delta_decode_step_noalloc", "delta_status_string"]
+            "delta_decode_step_noalloc", "delta_build_flags", "delta_status_string"]
+DELTA_BUILD_DEBUG = 1
+DELTA_DEBUG_PAGE, DELTA_DEBUG_SEQ_LEN, DELTA_DEBUG_SELECTION = 1, 2, 4
 DELTA_NOALLOC_SCRATCH_BYTES = 160 << 20
 
 
@@ -40,7 +44,8 @@ class delta_shape_t(ctypes.Structure):
 
 class delta_kv_t(ctypes.Structure):
     _fields_ = [("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
-                ("page_table", ctypes.c_void_p), ("seq_lens", ctypes.c_void_p)]
+                ("page_table", ctypes.c_void_p), ("seq_lens", ctypes.c_void_p),
+                ("n_pages", ctypes.c_int64)]
 
 
 class delta_select_t(ctypes.Structure):
@@ -81,6 +86,7 @@ def _bind(lib):
     lib.delta_decode_step_noalloc.argtypes = [_P(delta_shape_t), ctypes.c_int32, _P(ctypes.c_int32),
                                               _P(delta_kv_t), _P(_vp), _P(_vp), _P(delta_select_t),
                                               _vp, _vp, _vp]
+    lib.delta_build_flags.argtypes = []
     lib.delta_hbm_read_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, ctypes.c_int32, _vp]
     lib.delta_hbm_read_probe.restype = ctypes.c_int
     lib.delta_status_string.argtypes = [ctypes.c_int]
@@ -177,9 +183,18 @@ def make_kv(k_cache, v_cache, page_table, seq_lens) -> delta_kv_t:
     for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("page_table", page_table),
                     ("seq_lens", seq_lens)):
         _dev(name, t)
-    kv = delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr())
+    if k_cache.dim() < 1 or v_cache.dim() < 1 or k_cache.shape[0] != v_cache.shape[0]:
+        raise ValueError(f"k_cache and v_cache must hold the same number of pages "
+                         f"(got {tuple(k_cache.shape)}, {tuple(v_cache.shape)})")
+    kv = delta_kv_t(k_cache.data_ptr(), v_cache.data_ptr(), page_table.data_ptr(), seq_lens.data_ptr(),
+                    k_cache.shape[0])
     kv._tensors = (k_cache, v_cache, page_table, seq_lens)   # checked against the shape per call
     return kv
+
+
+def delta_build_flags() -> int:
+    """DELTA_BUILD_DEBUG if the loaded library is the debug build."""
+    return int(_lib.delta_build_flags())
 
 
 def delta_delta_path(shape: delta_shape_t, sel: delta_select_t) -> bool:

@@ -4,6 +4,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -24,7 +25,7 @@ def declared_functions(path=HEADER):
 
 def test_library_exports_every_declared_symbol(D):
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     lib = ctypes.CDLL(D.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -39,6 +40,25 @@ def test_probe_rejects_bad_arguments(D):
     assert lib.delta_hbm_read_probe(None, 1 << 20, fake, 64, 4, None) == -1
     assert lib.delta_hbm_read_probe(fake, 1 << 20, fake, 64, 3, None) == -1
     assert lib.delta_hbm_read_probe(ctypes.c_void_p(0x1001), 1 << 20, fake, 64, 4, None) == -1
+
+
+def test_build_flags(D):
+    """The library the binding loads is the release build; the debug build, where it has been
+    built (python -m paper_2510_09883_amd.build --debug), says so."""
+    if not os.environ.get("DELTA_ATTN_LIB"):
+        assert D.delta_build_flags() == 0
+    dbg = os.path.join(ROOT, "paper_2510_09883_amd", "libdelta_attn_debug.so")
+    if os.path.exists(dbg):
+        lib = ctypes.CDLL(dbg)
+        assert lib.delta_build_flags() == D.DELTA_BUILD_DEBUG
+
+
+def test_negative_page_count_is_refused(D):
+    s = shape(D)
+    kv = D.delta_kv_t(1, 2, 3, 4, -1)
+    fake = ctypes.c_void_p(0x1000)
+    need = D.delta_workspace_bytes(s)
+    assert D._lib.delta_full_attn(ctypes.byref(s), ctypes.byref(kv), fake, fake, fake, need, None) == -1
 
 
 def test_status_strings(D):
@@ -210,7 +230,7 @@ def test_binding_refuses_host_and_mistyped_buffers(D):
     with pytest.raises(ValueError, match="GPU tensor"):
         D.make_kv(k, k, pt, sl)
     with pytest.raises(TypeError):
-        D.make_kv(k.numpy(), k, pt, sl)
+        D.make_kv(np.zeros((4, 2, 16, 64)), k, pt, sl)
     # the per-call checks, on a descriptor built by hand (no tensors attached: skipped) and on
     # the q / out / selection buffers, which are always checked
     s = D.make_shape(1, 8, 2, 64, 4, 64)
