@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
     __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores are complete
     __syncthreads();
     if (tid == 0) {
-      const int prev = __hip_atomic_fetch_add(&a.counters[bg], 1, __ATOMIC_RELAXED,
+      const int prev = __hip_atomic_fetch_add(&a.counters[(size_t)bg * kCounterStride], 1, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT);
       s_last = prev == n_valid - 1;
     }
@@ -367,7 +367,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(const AttnArgs a) {
       M = Mn;
     }
     store_out(O, L, M);
-    if (tid == 0) __hip_atomic_store(&a.counters[bg], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&a.counters[(size_t)bg * kCounterStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
 
   // ---- which pieces this workgroup attends to --------------------------------------------

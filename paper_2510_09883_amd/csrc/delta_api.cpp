@@ -204,7 +204,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
   }
   size_t off = 0;
   L->status = off;    off = align_up(off + sizeof(uint32_t));   // debug builds' status word
-  L->counters = off;  off = align_up(off + sizeof(int32_t) * pairs);
+  L->counters = off;  off = align_up(off + sizeof(int32_t) * (size_t)pairs * kCounterStride);
   L->part_ml = off;   off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * 2);
   L->part_o = off;    off = align_up(off + sizeof(float) * (size_t)pairs * part_splits * G * s->head_dim);
   if (sel) {
@@ -213,7 +213,7 @@ int make_layout(const delta_shape_t* s, const delta_select_t* sel, Layout* L) {
     L->lse = off;     off = align_up(off + sizeof(float) * (size_t)s->batch * s->n_q_heads);
     L->uscores = off; off = align_up(off + sizeof(float) * (size_t)s->batch * L->nu_stride);
     L->phys = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * (sel->budget_tokens / sel->unit_tokens));
-    L->fcnt = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * 3);
+    L->fcnt = off;    off = align_up(off + sizeof(int32_t) * (size_t)s->batch * kCounterStride);
     L->fflag = off;   off = align_up(off + sizeof(int32_t) * (size_t)s->batch * L->fused_chunks);
   }
   L->total = off;
@@ -591,10 +591,9 @@ int delta_decode_step_noalloc(const delta_shape_t* shape, int32_t n_layers, cons
   // shape; the arrival counters of this call's layout must start at zero (every other region is
   // written before it is read, and the kernels re-arm the counters they use).
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const size_t pairs = (size_t)shape->batch * shape->n_kv_heads;
   const size_t fused_bytes = L.fcnt ? L.total - L.fcnt : 0;   // fused counters and chunk flags
   // (from byte 0: the debug builds' status word, then the counters)
-  if (launch_fill_zero2(w, L.counters + sizeof(int32_t) * pairs, w + L.fcnt, fused_bytes, st) != hipSuccess)
+  if (launch_fill_zero2(w, L.part_ml, w + L.fcnt, fused_bytes, st) != hipSuccess)
     return DELTA_ERR_HIP;
   return enqueue_step(shape, n_layers, roles, kv, q, out, sel, sel_idx, sel_cnt, L, w, stream,
                       nullptr);

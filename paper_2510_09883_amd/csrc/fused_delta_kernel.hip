@@ -139,11 +139,13 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
   __syncthreads();
   __shared__ int s_ok;
   if (tid == 0) {
-    __hip_atomic_fetch_add(&a.counters[3 * b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the last workgroup to arrive learns it from its own count and does not poll
+    const int before = __hip_atomic_fetch_add(&a.counters[(size_t)b * kCounterStride], 1, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    int ok = 0;
-    for (int it = 0; it < kSpinLimit; ++it) {
-      if (__hip_atomic_load(&a.counters[3 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_active) {
+    int ok = before + 1 >= n_active;
+    for (int it = 0; !ok && it < kSpinLimit; ++it) {
+      if (__hip_atomic_load(&a.counters[(size_t)b * kCounterStride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n_active) {
         ok = 1;
         break;
       }
@@ -300,13 +302,24 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
   };
 
   int32_t* deferred = a.chunk_flags + (size_t)b * a.n_chunks;
+  // counts this workgroup in for step 6 once its stores are complete (s_last: it is the last)
+  auto arrive = [&]() {
+    __builtin_amdgcn_s_waitcnt(0);   // this thread's score / logit / flag stores are complete
+    __syncthreads();
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(&a.counters[(size_t)b * kCounterStride + 32], 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) == n_active - 1;
+  };
   if (ok) {
     // the log-sum-exp loads (wave 0) and the first merge pass's loads (waves 1-3) are in flight
-    // together; the chunk is scored before the merge arithmetic, so the page scores leave first
+    // together; the chunk is scored before the merge arithmetic, so the page scores leave
+    // first, and the workgroup counts itself in for the selection as soon as they are complete
+    // (the merge's loads are complete by then too; its output stores are not waited for)
     merge_outputs(c, [&]() {
       lse_heads();
       lds_barrier();   // s_M, s_L, s_lse; the merge loads stay in flight
       score_chunk(c, true);
+      arrive();
     });
   } else {
     // leave the chunk to the sequence's last workgroup: its logits go to the workspace
@@ -318,22 +331,18 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
     }
     if (tid == 0) {
       __hip_atomic_store(deferred + c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.counters[3 * b + 2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.counters[(size_t)b * kCounterStride + 48], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 
   // ---- 6. the last workgroup of the sequence finishes left chunks and selects --------------
-  __builtin_amdgcn_s_waitcnt(0);   // this thread's score / logit / flag stores are complete
-  __syncthreads();
-  if (tid == 0)
-    s_last = __hip_atomic_fetch_add(&a.counters[3 * b + 1], 1, __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT) == n_active - 1;
+  if (!ok) arrive();
   __syncthreads();
   if (!s_last) return;
   // every workgroup of the sequence has arrived (so every partial is stored) and has either
   // scored its chunk or left it
   __shared__ int s_flag;
-  if (tid == 0) s_flag = __hip_atomic_load(&a.counters[3 * b + 2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) s_flag = __hip_atomic_load(&a.counters[(size_t)b * kCounterStride + 48], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (s_flag) {
     if (!ok) compute_lse();
@@ -352,9 +361,9 @@ __global__ __launch_bounds__(kAttnThreads) void fused_delta_kernel(const FusedAr
   }
   select_sequence<kFusedKeysPerThread, U>(a.sel, b);
   if (tid == 0) {
-    __hip_atomic_store(&a.counters[3 * b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&a.counters[3 * b + 1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&a.counters[3 * b + 2], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[(size_t)b * kCounterStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[(size_t)b * kCounterStride + 32], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.counters[(size_t)b * kCounterStride + 48], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 

@@ -29,6 +29,9 @@ constexpr int kMaxRowSlots = 1024;       // LDS slots staging a split's page / r
 constexpr int kMaxGroup = 8;             // query heads per KV head (padded to 16 MFMA columns)
 constexpr int kMaxSelectKeys = 8192;     // candidate units one selection workgroup holds in registers
 constexpr int kBalanceMaxBatch = 64;     // sequences of a balanced dense launch (one per lane)
+// Ints between consecutive arrival counters (256 bytes): every counter that many workgroups
+// update and poll sits in a memory block of its own instead of sharing one with its neighbours'.
+constexpr int kCounterStride = 64;
 
 struct AttnArgs {
   const uint16_t* k_cache;   // bf16 [pages, Hkv, 16, D]
@@ -42,7 +45,7 @@ struct AttnArgs {
   uint16_t* out;             // bf16 [B, Hq, D]
   float* part_o;             // [B*Hkv, slots, G, D]   un-normalised partial outputs
   float* part_ml;            // [B*Hkv, slots, G, 2]   partial (max, sum) in the log2 domain
-  int32_t* counters;         // [B*Hkv] arrival counters, zero between launches
+  int32_t* counters;         // [B*Hkv] arrival counters (kCounterStride apart), zero between launches
   float* logits;             // [B, Hkv, logit_pages, G, 16] log2-domain logits, or null
   float* lse;                // [B, Hq] log2-domain log-sum-exp, or null
   int64_t page_stride;       // elements per physical page = Hkv * 16 * D
@@ -103,8 +106,9 @@ struct FusedArgs {
   uint16_t* out;             // bf16 [B, Hq, D]
   float* part_o;             // [B, Hkv, n_chunks, G, D]  un-normalised chunk outputs
   float* part_ml;            // [B, Hkv, n_chunks, G, 2]  chunk (max, sum), log2 domain
-  int32_t* counters;         // [B, 3] arrivals after attention, arrivals after scoring, "a
-                             // chunk was left to the last workgroup"; zero between launches
+  int32_t* counters;         // [B] x kCounterStride: arrivals after attention (int 0 of each
+                             // sequence's block), arrivals after scoring (int 32), "a chunk was
+                             // left to the last workgroup" (int 48); zero between launches
   int32_t* chunk_flags;      // [B, n_chunks] chunk left to the last workgroup; zero between launches
   float* logits;             // [B, Hkv, logit_pages, G, 16] logits of left chunks (workspace)
   float* unit_scores;        // [B, sel.nu_stride] page (or token) scores, written here
