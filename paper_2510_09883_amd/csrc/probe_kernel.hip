@@ -45,6 +45,41 @@ __global__ __launch_bounds__(256) void read_probe_kernel(const u32x4* __restrict
   }
 }
 
+// Gather of 4 KB chunks (delta_hbm_gather_probe): the workgroup's chunk list goes to LDS, then
+// every thread walks the list with a ring of three 16-byte loads (the loads of the next two
+// chunks in flight while one is folded in), as a wave of the attention kernel walks its tiles.
+constexpr int kGatherMaxChunks = 4096;
+constexpr int kGatherRing = 3;
+
+__global__ __launch_bounds__(256) void gather_probe_kernel(const u32x4* __restrict__ src,
+                                                           const int64_t* __restrict__ chunks,
+                                                           int n_chunks,
+                                                           uint32_t* __restrict__ sink) {
+  __shared__ int64_t s_list[kGatherMaxChunks];
+  const int w = blockIdx.x, W = gridDim.x, t = threadIdx.x;
+  const int c0 = (int)((int64_t)n_chunks * w / W), c1 = (int)((int64_t)n_chunks * (w + 1) / W);
+  const int nc = c1 - c0;   // <= kGatherMaxChunks (checked on the host)
+  for (int i = t; i < nc; i += 256) s_list[i] = chunks[c0 + i];
+  __syncthreads();
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  if (nc > 0) {
+    u32x4 v[kGatherRing];
+    auto fetch = [&](u32x4& x, int k) {
+      x = __builtin_nontemporal_load(src + s_list[k < nc ? k : nc - 1] * 256 + t);
+    };
+#pragma unroll
+    for (int i = 0; i < kGatherRing - 1; ++i) fetch(v[i], i);
+    for (int k = 0; k < nc; k += kGatherRing) {
+#pragma unroll
+      for (int r = 0; r < kGatherRing; ++r) {
+        fetch(v[(r + kGatherRing - 1) % kGatherRing], k + r + kGatherRing - 1);
+        if (k + r < nc) acc ^= v[r];
+      }
+    }
+  }
+  sink[(size_t)w * 256 + t] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+
 }  // namespace
 
 #pragma GCC visibility push(default)
@@ -63,6 +98,18 @@ extern "C" int delta_hbm_read_probe(const void* buf, size_t bytes, uint32_t* sin
     case 8: hipLaunchKernelGGL(read_probe_kernel<8>, grid, block, 0, st, src, n, sink); break;
     default: return -1;
   }
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+extern "C" int delta_hbm_gather_probe(const void* buf, size_t bytes, const int64_t* chunks,
+                                      int32_t n_chunks, uint32_t* sink, int32_t n_workgroups,
+                                      void* stream) {
+  if (!buf || !chunks || !sink || bytes < 4096 || n_chunks < 1 || n_workgroups < 1 ||
+      (reinterpret_cast<uintptr_t>(buf) & 15) ||
+      ((int64_t)n_chunks + n_workgroups - 1) / n_workgroups > kGatherMaxChunks)
+    return -1;
+  hipLaunchKernelGGL(gather_probe_kernel, dim3(n_workgroups), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const u32x4*>(buf), chunks,
+                     n_chunks, sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 #pragma GCC visibility pop

@@ -89,6 +89,9 @@ def _bind(lib):
     lib.delta_build_flags.argtypes = []
     lib.delta_hbm_read_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, ctypes.c_int32, _vp]
     lib.delta_hbm_read_probe.restype = ctypes.c_int
+    lib.delta_hbm_gather_probe.argtypes = [_vp, ctypes.c_size_t, _vp, ctypes.c_int32, _vp,
+                                           ctypes.c_int32, _vp]
+    lib.delta_hbm_gather_probe.restype = ctypes.c_int
     lib.delta_status_string.argtypes = [ctypes.c_int]
     lib.delta_status_string.restype = ctypes.c_char_p
     for n in EXPORTED[:-1]:
@@ -364,3 +367,18 @@ def delta_hbm_read_probe(buf, sink, n_workgroups=2048, unroll=4):
     rc = _lib.delta_hbm_read_probe(_ptr(buf), _nbytes(buf), _ptr(sink), n_workgroups, unroll, _stream())
     if rc != 0:
         raise DeltaError("delta_hbm_read_probe", rc)
+
+
+def delta_hbm_gather_probe(buf, chunks, sink, n_workgroups=256):
+    """Gather of the 4 KB chunks `chunks` (int64, device) of `buf` (include/delta_probe.h);
+    sink: int32/uint32 [n_workgroups * 256].  Every chunk index must lie inside `buf`: checked
+    here (a device-to-host read) except while the stream is being captured into a graph, where
+    the caller must have made the same call eagerly first."""
+    n = _nbytes(buf) // 4096
+    if not torch.cuda.is_current_stream_capturing() and chunks.numel() and \
+            (int(chunks.min()) < 0 or int(chunks.max()) >= n):
+        raise ValueError("gather probe: chunk index outside the buffer")
+    rc = _lib.delta_hbm_gather_probe(_ptr(buf), _nbytes(buf), _ptr(chunks), chunks.numel(), _ptr(sink),
+                                     n_workgroups, _stream())
+    if rc != 0:
+        raise DeltaError("delta_hbm_gather_probe", rc)

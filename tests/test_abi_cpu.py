@@ -31,7 +31,8 @@ def test_library_exports_every_declared_symbol(D):
         assert hasattr(lib, n), n
     assert sorted(D.EXPORTED) == names
     probe = declared_functions(PROBE_HEADER)
-    assert probe == ["delta_hbm_read_probe"] and hasattr(lib, probe[0])
+    assert probe == ["delta_hbm_gather_probe", "delta_hbm_read_probe"]
+    assert all(hasattr(lib, n) for n in probe)
 
 
 def test_probe_rejects_bad_arguments(D):
@@ -40,6 +41,12 @@ def test_probe_rejects_bad_arguments(D):
     assert lib.delta_hbm_read_probe(None, 1 << 20, fake, 64, 4, None) == -1
     assert lib.delta_hbm_read_probe(fake, 1 << 20, fake, 64, 3, None) == -1
     assert lib.delta_hbm_read_probe(ctypes.c_void_p(0x1001), 1 << 20, fake, 64, 4, None) == -1
+    g = lib.delta_hbm_gather_probe
+    assert g(None, 1 << 20, fake, 16, fake, 4, None) == -1           # no buffer
+    assert g(fake, 1 << 20, None, 16, fake, 4, None) == -1           # no chunk list
+    assert g(fake, 1 << 20, fake, 0, fake, 4, None) == -1            # nothing to read
+    assert g(fake, 1 << 20, fake, 4096 * 4 + 1, fake, 4, None) == -1  # > 4096 chunks per workgroup
+    assert g(ctypes.c_void_p(0x1001), 1 << 20, fake, 16, fake, 4, None) == -1
 
 
 def test_build_flags(D):
