@@ -178,28 +178,20 @@ def read_ceiling(D):
             "kernel": "delta_hbm_read_probe (16-byte streaming loads)"}
 
 
-def gather_ceiling(D, nbytes, steps=20):
-    """The time and rate of a plain gather of `nbytes` in random 4 KB chunks (the probe kernel
-    of include/delta_probe.h, the page-tile access pattern of the sparse layers) out of a 4 GiB
-    buffer, by 256 workgroups: per-launch time from a graph of 8 launches replayed `steps`
-    times, as the layers are timed.  The floor of a sparse layer that moves those bytes."""
-    span = 4 << 30
-    buf = torch.ones(span // 4, dtype=torch.int32, device="cuda")
-    n = max(1, int(round(nbytes / 4096)))
-    g = torch.Generator().manual_seed(4096)
-    chunks = torch.randint(0, span // 4096, (n,), generator=g, dtype=torch.int64).cuda()
-    sink = torch.zeros(256 * 256, dtype=torch.int32, device="cuda")
+def _graph_us(launch, steps):
+    """Per-launch time of `launch()` from a graph of 8 launches replayed `steps` times (after
+    two eager launches on a side stream), as the layers are timed."""
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         for _ in range(2):
-            D.delta_hbm_gather_probe(buf, chunks, sink, 256)
+            launch()
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         for _ in range(8):
-            D.delta_hbm_gather_probe(buf, chunks, sink, 256)
+            launch()
     graph.replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -208,12 +200,39 @@ def gather_ceiling(D, nbytes, steps=20):
         graph.replay()
     e1.record()
     torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / (steps * 8)
-    del buf
+    return e0.elapsed_time(e1) * 1e3 / (steps * 8)
+
+
+def gather_ceiling(D, nbytes, steps=20):
+    """The time and rate of a plain gather of `nbytes` in random 4 KB chunks (the probe kernel
+    of include/delta_probe.h, the page-tile access pattern of the sparse layers) out of a 4 GiB
+    buffer, by 256 workgroups, and of a plain streaming read of the same number of contiguous
+    bytes (best of a few launch shapes), both timed per launch as the layers are: the floors of
+    a sparse layer that moves those bytes, the second one's for any kernel that reads them."""
+    span = 4 << 30
+    buf = torch.ones(span // 4, dtype=torch.int32, device="cuda")
+    n = max(1, int(round(nbytes / 4096)))
+    g = torch.Generator().manual_seed(4096)
+    chunks = torch.randint(0, span // 4096, (n,), generator=g, dtype=torch.int64).cuda()
+    sink = torch.zeros(256 * 256, dtype=torch.int32, device="cuda")
+    D.delta_hbm_gather_probe(buf, chunks, sink, 256)   # eager first: checks the chunk indices
+    us = _graph_us(lambda: D.delta_hbm_gather_probe(buf, chunks, sink, 256), steps)
+    sub = buf[: n * 1024]
+    stream = None
+    for wgs in (256, 512, 1024):
+        for unroll in (4, 8):
+            t = _graph_us(lambda: D.delta_hbm_read_probe(sub, sink, wgs, unroll), steps)
+            if stream is None or t < stream[0]:
+                stream = (t, f"{wgs} workgroups, {unroll} loads in flight per thread")
+    del buf, sub
     torch.cuda.empty_cache()
     return {"gbps": round(n * 4096 / (us * 1e-6) / 1e9, 1), "us_per_launch": round(us, 2),
             "bytes": n * 4096, "pattern": "random 4 KB chunks of a 4 GiB buffer, 256 workgroups",
-            "kernel": "delta_hbm_gather_probe (16-byte streaming loads, two chunks in flight per thread)"}
+            "kernel": "delta_hbm_gather_probe (16-byte streaming loads, two chunks in flight per thread)",
+            "stream_same_bytes": {"us_per_launch": round(stream[0], 2),
+                                  "gbps": round(n * 4096 / (stream[0] * 1e-6) / 1e9, 1),
+                                  "launch": stream[1],
+                                  "kernel": "delta_hbm_read_probe over the same number of contiguous bytes"}}
 
 
 def time_layers(D, w, sets, stack, shape, sel, ws, steps, other_sel=None):
@@ -967,7 +986,8 @@ def main():
         "layer_frac_of_measured_ceiling": {k: round(role_bytes[k] / (layer_us[k] * 1e-6) / 1e9 / ceiling["gbps"], 4)
                                            for k in layer_us},
         "sparse_gather_floor": None if gather is None or "sparse" not in layer_us else dict(
-            gather, sparse_layer_over_floor=round(layer_us["sparse"] / gather["us_per_launch"], 4)),
+            gather, sparse_layer_over_floor=round(layer_us["sparse"] / gather["us_per_launch"], 4),
+            sparse_layer_over_stream=round(layer_us["sparse"] / gather["stream_same_bytes"]["us_per_launch"], 4)),
         "delta_select_overhead": None if overhead is None else round(overhead, 4),
         "delta_path": None if configs.ROLE_DELTA not in w.roles else ("fused" if step_fused else "split"),
         "delta_other_path": None if other_us is None else {
